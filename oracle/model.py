@@ -15,12 +15,13 @@ and an untied lm_head; no biases, no embedding scale.
 Weight matrices are stored [out, in] (a linear map is x @ W^T).  All arithmetic
 is float64; the bf16 weights of bf16 models are exactly representable.
 
-Operand precision.  ``operands="exact"`` is the pure float64 definition.
-``operands="bf16"`` is the bfloat16 model: every matrix product takes bf16
-operands (its activation input is rounded to nearest-even bf16 first; the
-weights already are bf16) and the key/value cache stores bf16 (keys rounded
-after RoPE).  Everything else -- residual stream, norms, RoPE, attention scores,
-softmax, the query, and every accumulation -- stays float64.
+Storage precision.  A model's matrices and its key/value cache are stored in
+the model's dtype (fp32 or bf16); every other value -- activations entering a
+matrix product, residual stream, norms, RoPE, queries, attention scores,
+softmax and every accumulation -- is exact here (float64).  So a bf16 model
+computes with bf16 weights (exactly representable) and reads back keys and
+values rounded to nearest-even in the storage type (keys after RoPE).
+``kv_storage="exact"`` keeps the cache in float64 (the pure definition).
 """
 from __future__ import annotations
 
@@ -30,11 +31,13 @@ import numpy as np
 
 
 class OracleModel:
-    def __init__(self, shape, weights, cache_f64: bool = True, operands: str = "exact"):
-        if operands not in ("exact", "bf16"):
-            raise ValueError(operands)
+    def __init__(self, shape, weights, cache_f64: bool = True, kv_storage: str = "model"):
+        if kv_storage == "model":
+            kv_storage = shape.dtype
+        if kv_storage not in ("exact", "f32", "bf16"):
+            raise ValueError(kv_storage)
         self.s = shape
-        self.bf16 = operands == "bf16"
+        self.kv_storage = kv_storage
         cv = (lambda a: np.asarray(a, np.float64)) if cache_f64 else (lambda a: a)
         self.embed = cv(weights.embed)
         self.final_norm = np.asarray(weights.final_norm, np.float64)
@@ -57,14 +60,17 @@ class OracleModel:
         m, e = np.frexp(np.asarray(x, np.float64))          # x = m * 2**e, 0.5 <= |m| < 1
         return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
 
-    def linear(self, x: np.ndarray, w: np.ndarray) -> np.ndarray:
-        x = np.asarray(x, np.float64)
-        if self.bf16:
-            x = self.round_bf16(x)
-        return x @ np.asarray(w, np.float64).T
+    @staticmethod
+    def linear(x: np.ndarray, w: np.ndarray) -> np.ndarray:
+        return np.asarray(x, np.float64) @ np.asarray(w, np.float64).T
 
     def kv_store(self, a: np.ndarray) -> np.ndarray:
-        return self.round_bf16(a) if self.bf16 else a
+        """The value the cache holds for a freshly computed key or value."""
+        if self.kv_storage == "bf16":
+            return self.round_bf16(a)
+        if self.kv_storage == "f32":
+            return np.asarray(a, np.float32).astype(np.float64)
+        return a
 
     def rope(self, x: np.ndarray, pos: np.ndarray) -> np.ndarray:
         """x: [T, H, hd]; pos: [T] integer positions."""

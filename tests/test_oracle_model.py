@@ -24,7 +24,7 @@ GQA = ModelShape(2, 64, 6, 2, 16, 96, 97, 1e4, dtype="f32")     # 3 q heads per 
 
 
 def _model(shape, seed=0):
-    return OracleModel(shape, make_weights(shape, seed))
+    return OracleModel(shape, make_weights(shape, seed), kv_storage="exact")
 
 
 def torch_forward(shape, w, tokens):
@@ -58,7 +58,7 @@ def torch_forward(shape, w, tokens):
 @pytest.mark.parametrize("shape", [TINY, GQA], ids=["tiny", "gqa"])
 def test_forward_matches_torch_functional(shape):
     w = make_weights(shape, 1)
-    m = OracleModel(shape, w)
+    m = OracleModel(shape, w, kv_storage="exact")
     toks = np.random.default_rng(2).integers(0, shape.vocab - 1, size=21)
     ours = m.forward(toks, np.arange(len(toks)), m.new_cache())
     ref = torch_forward(shape, w, toks)
@@ -123,3 +123,34 @@ def test_decode_batch_equals_single():
     for i in range(3):
         zi = m.forward(toks[i:i + 1], pos[i:i + 1], caches_b[i])[0]
         np.testing.assert_allclose(zb[i], zi, rtol=0, atol=1e-12)
+
+
+def test_round_bf16_matches_torch_and_ties_to_even():
+    x = np.random.default_rng(0).normal(size=100000).astype(np.float32).astype(np.float64)
+    ours = OracleModel.round_bf16(x)
+    ref = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(ours, ref)
+    # halfway cases go to the even neighbour; anything above half rounds up
+    np.testing.assert_array_equal(OracleModel.round_bf16(np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8),
+                                                                     1 + 2 ** -8 + 2 ** -30])),
+                                  [1.0, 1 + 2 ** -6, -1.0, 1 + 2 ** -7])
+
+
+def test_kv_storage_modes():
+    bshape = ModelShape(2, 64, 4, 2, 16, 96, 97, 1e4, dtype="bf16")
+    w = make_weights(bshape, 2)
+    toks = np.random.default_rng(3).integers(0, 96, size=12)
+    m = OracleModel(bshape, w)                       # bf16 cache
+    c = m.new_cache()
+    full = m.forward(toks, np.arange(12), c)
+    for layer in c:                                  # every cached value is a bf16 number
+        np.testing.assert_array_equal(layer["k"], OracleModel.round_bf16(layer["k"]))
+        np.testing.assert_array_equal(layer["v"], OracleModel.round_bf16(layer["v"]))
+    # KV-cached decode still equals full recompute with the same storage rule
+    c2 = m.new_cache()
+    m.forward(toks[:7], np.arange(7), c2)
+    for i in range(7, 12):
+        np.testing.assert_allclose(m.forward(toks[i:i + 1], np.array([i]), c2)[0], full[i], rtol=0, atol=1e-11)
+    ex = OracleModel(bshape, w, kv_storage="exact")
+    d = np.abs(ex.forward(toks, np.arange(12), ex.new_cache()) - full).max()
+    assert 0 < d < 5e-2                              # storage rounding moves logits a little
