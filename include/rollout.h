@@ -1,0 +1,227 @@
+/*
+ * rollout.h -- C ABI of librollout.so, the MI355X (gfx950) group-rollout library.
+ *
+ * What it computes.  Synchronous GRPO/DAPO training samples, for every prompt,
+ * a group of G completions, scores them and forms group-relative advantages
+ * (paper Sec. 3.1, problem statement; Sec. 4, requirements (i)-(iii)).  The
+ * batched generation of such groups is gated by the longest completion of each
+ * group (Sec. 3.1, Eq. ratio) and is the part of the training step this
+ * library runs on the GPU:
+ *
+ *   rollout_group    -- prefill every prompt once, fork its G siblings over a
+ *                       shared prompt prefix in a paged KV cache, then decode
+ *                       all siblings together, sampling each token by
+ *                       Gumbel-max from a Philox4x64-10 stream and retiring
+ *                       every sequence at its EOS.
+ *   group_advantage  -- A_i = (r_i - mean_g r) / (std_g r + eps) per group.
+ *
+ * Conventions for every entry point.
+ *   - Status: 0 on success, a negative RG_E* code on error; rg_last_error()
+ *     then returns a message (thread-local, valid until the next call made
+ *     by the same thread).  No exception crosses the ABI.  Outputs are
+ *     undefined after an error.
+ *   - "device" pointers are HIP device memory of the current device; "host"
+ *     pointers are ordinary CPU memory read before the call returns.
+ *   - `stream` is a hipStream_t passed as void*.  NULL is the null stream.
+ *   - Integer ids and sizes are int32 unless stated; tensors are dense,
+ *     row-major, with the shapes given in brackets.
+ */
+#ifndef PAPER_2606_02218_ROLLOUT_H
+#define PAPER_2606_02218_ROLLOUT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---- */
+#define RG_OK            0
+#define RG_EINVAL       (-1)  /* an argument is out of range or inconsistent            */
+#define RG_ENOMEM       (-2)  /* a size exceeds the policy's limits or its KV page pool  */
+#define RG_EHIP         (-3)  /* a HIP runtime call failed                             */
+#define RG_EUNSUPPORTED (-4)  /* a model shape the kernels do not handle              */
+
+/* ---- element types ---- */
+#define RG_DTYPE_F32  0
+#define RG_DTYPE_BF16 1
+
+/* Decoder shape.  Pre-norm blocks x += Attn(RMSNorm(x)), x += MLP(RMSNorm(x)),
+ * final RMSNorm, untied lm_head, no biases.  RMSNorm(x) = x/sqrt(mean(x^2)+eps)*g.
+ * RoPE rotates dims (i, i+head_dim/2) by pos*rope_theta^(-2i/head_dim); prompt
+ * tokens are at positions 0..Lp-1, generated token t at Lp+t.  Query head h
+ * reads key/value head floor(h*n_kv_heads/n_q_heads).  MLP =
+ * W_down(silu(W_gate x) * (W_up x)).
+ * Supported: head_dim even and <= 256, n_q_heads a multiple of n_kv_heads,
+ * d_model, n_q_heads*head_dim and ffn_dim multiples of 32, vocab a multiple
+ * of 16 (otherwise RG_EUNSUPPORTED). */
+typedef struct rg_config {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  int32_t eos_id;       /* token that ends a completion, in [0, vocab)                   */
+  float rope_theta;
+  float rms_eps;
+  int32_t dtype;        /* RG_DTYPE_F32: fp32 matrices and KV.  RG_DTYPE_BF16: bf16
+                           matrices and KV, bf16 GEMM operands (activations rounded to
+                           nearest-even bf16 at each matrix-product input, keys after
+                           RoPE), fp32 residual, norms, attention and accumulation.      */
+} rg_config;
+
+/* Weights, all DEVICE pointers, read during rg_policy_create only (the policy
+ * keeps its own repacked copy; the caller may free these afterwards).
+ * Matrices are [out, in] row-major (y = x W^T) in the config dtype; norm gains
+ * are always fp32.  The per-layer members are HOST arrays of n_layers device
+ * pointers. */
+typedef struct rg_weights {
+  const void* embed;               /* [vocab, d_model]                  */
+  const void* final_norm;          /* [d_model] fp32                    */
+  const void* lm_head;             /* [vocab, d_model]                  */
+  const void* const* attn_norm;    /* [d_model] fp32                    */
+  const void* const* wq;           /* [n_q_heads*head_dim, d_model]     */
+  const void* const* wk;           /* [n_kv_heads*head_dim, d_model]    */
+  const void* const* wv;           /* [n_kv_heads*head_dim, d_model]    */
+  const void* const* wo;           /* [d_model, n_q_heads*head_dim]     */
+  const void* const* ffn_norm;     /* [d_model] fp32                    */
+  const void* const* w_gate;       /* [ffn_dim, d_model]                */
+  const void* const* w_up;         /* [ffn_dim, d_model]                */
+  const void* const* w_down;       /* [d_model, ffn_dim]                */
+} rg_weights;
+
+/* Capacity of a policy, fixed at creation: the device workspace (activations,
+ * logits, attention partials) and the KV page pool are allocated once. */
+typedef struct rg_limits {
+  int32_t max_seqs;           /* largest N = sum(G) of one rollout                        */
+  int32_t max_prompts;        /* largest P                                                */
+  int32_t max_prompt_tokens;  /* largest sum of prompt lengths                            */
+  int32_t max_context;        /* largest prompt length + max_new                          */
+  int64_t kv_pool_pages;      /* KV pages in the pool; 0 = enough for the worst case of
+                                 the other limits (every sequence reaching max_context)   */
+} rg_limits;
+
+typedef struct rg_policy rg_policy;  /* opaque: packed weights, KV pool, workspace */
+
+/* Flags for rg_sampling.flags */
+#define RG_FLAG_NO_PREFIX_SHARING 1  /* give every sibling private copies of its prompt's
+                                        KV pages (results are bit-identical; a test aid) */
+#define RG_FLAG_PROFILE           2  /* time every kernel launch with HIP events; read the
+                                        totals with rg_kernel_times()                    */
+
+/* Sampling options.  A NULL rg_sampling* means temperature 1, natural EOS, no
+ * flags.  Token t of sequence s is argmax_v fp32(z_v/T) + g_v where g_v is the
+ * fp32 Gumbel variate -log(-log(u)) of the stream documented at
+ * rg_gumbel_bits() for (seed, t, s, v); ties go to the lowest id.  With
+ * forced_len, EOS scores -inf while t < forced_len[s]-1 and token
+ * forced_len[s]-1 is EOS (the synthetic stand-in for a policy's own stopping
+ * time).  The reported log-probability is that of the emitted token under the
+ * unmasked softmax(z/T). */
+typedef struct rg_sampling {
+  float temperature;            /* > 0                                                      */
+  int32_t flags;                /* RG_FLAG_*                                                */
+  const int32_t* forced_len;    /* HOST [N] in [1, max_new], or NULL for natural EOS       */
+  const int32_t* force_tokens;  /* DEVICE [N*max_new] or NULL.  Teacher forcing: the token
+                                   fed to step t+1 is force_tokens[s*max_new+t] (retirement
+                                   follows it), `tokens` still receives the library's own
+                                   sampling decision and `logprobs` the forced token's.    */
+  float* dump_logits;           /* DEVICE [dump_steps*N*vocab] or NULL: raw logits z of
+                                   sequence s at step t < dump_steps go to
+                                   dump_logits[(t*N+s)*vocab ...]; untouched otherwise     */
+  int32_t dump_steps;
+} rg_sampling;
+
+const char* rg_last_error(void);
+
+/* Create a policy for one decoder.  Validates the shape, copies and repacks
+ * the weights, allocates the workspace and KV pool for `limits` on the current
+ * device.  *out receives the handle.  Errors: RG_EINVAL (NULL arguments,
+ * non-positive sizes), RG_EUNSUPPORTED (shape), RG_ENOMEM / RG_EHIP
+ * (allocation). */
+int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits* limits,
+                     rg_policy** out);
+void rg_policy_destroy(rg_policy* pol);   /* NULL is a no-op */
+
+/* Bytes of device memory the policy holds (weights + workspace + KV pool). */
+int64_t rg_policy_device_bytes(const rg_policy* pol);
+
+/* Generate G[p] completions for each prompt p (paper Sec. 3.1).
+ *   prompts     DEVICE int32 [sum(prompt_len)], prompts packed back to back; ids in
+ *               [0, vocab)
+ *   prompt_len  HOST   int32 [P], each >= 1
+ *   G           HOST   int32 [P], each >= 1; N = sum(G)
+ *   max_new     >= 1; prompt_len[p] + max_new <= limits.max_context
+ *   seed        Philox key word 0 of the sampling stream
+ * Sequence s = off_p + j (off = exclusive prefix sum of G) is sibling j of
+ * prompt p.  Outputs (caller-allocated DEVICE buffers):
+ *   tokens    int32 [N*max_new]: tokens[s*max_new+t]; -1 after the completion
+ *   lengths   int32 [N]: generated tokens including the final EOS (or max_new)
+ *   logprobs  fp32  [N*max_new]: log-probability of each emitted token; 0 after
+ * Work is enqueued on `stream`; the call returns once every sequence has
+ * retired (it reads the active count back from the device), so the outputs
+ * are complete when the stream's work is.  Not thread-safe per policy.
+ * Errors: RG_EINVAL (arguments), RG_ENOMEM (N, P, prompt tokens or context
+ * beyond the limits, or the KV page pool ran out during decoding), RG_EHIP. */
+int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_len, int32_t P,
+                  const int32_t* G, int32_t max_new, uint64_t seed, const rg_sampling* opts,
+                  int32_t* tokens, int32_t* lengths, float* logprobs, void* stream);
+
+/* Group-relative advantage (paper Sec. 3.1: group-relative baseline from the
+ * group's mean and standardized rewards).  For each group p of G[p] rewards:
+ * mean and std (std with `ddof`, 0 or 1) in fp64, A = (r - mean)/(std + eps)
+ * rounded to fp32; a group whose rewards are all equal, or with G[p] <= ddof,
+ * gets A = 0.
+ *   rewards  DEVICE fp32 [N], groups back to back (N = sum(G))
+ *   G        DEVICE int32 [P], each >= 1 (read by the kernel)
+ *   adv      DEVICE fp32 [N] (may not alias rewards)
+ * Only enqueues work on `stream`; allocates nothing.  Errors: RG_EINVAL for
+ * P < 1, N < 1, eps < 0 or ddof not in {0, 1}; a G[] entry < 1 or a sum that
+ * differs from N makes the kernel write NaN to adv[0].  */
+int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N, float eps,
+                    int32_t ddof, float* adv, void* stream);
+
+/* ---- test and measurement hooks ---- */
+
+/* Raw Philox4x64-10 blocks: out[4i..4i+3] = Philox(ctr[4i..4i+3], key (key0, key1)).
+ * ctr and out are DEVICE uint64 [4n].  Enqueue only. */
+int rg_philox_blocks(uint64_t key0, uint64_t key1, const uint64_t* ctr, int64_t n, uint64_t* out,
+                     void* stream);
+
+/* The 32-bit values the sampler draws for sequence s at step t: out[v] for
+ * v < vocab, from block Philox((v>>3, t, s, 0), (seed, 1)), 32-bit half (v&1)
+ * (low first) of 64-bit word ((v&7)>>1).  out is DEVICE uint32 [vocab]. */
+int rg_gumbel_bits(uint64_t seed, int32_t t, int32_t s, int32_t vocab, uint32_t* out, void* stream);
+
+/* Per-step record of the last rollout_group call: active[t] = sequences still
+ * decoding at step t (t = 0 is the first sampled token), groups[t] = prompts
+ * with at least one of them, ctx[t] = sum over those sequences of their prompt
+ * length.  Each array is HOST [cap]; *n_steps receives the number of steps
+ * (the longest completion), at most cap entries are written.  Any array may be
+ * NULL. */
+int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t* active,
+                    int32_t* groups, int64_t* ctx);
+
+/* Kernel classes timed under RG_FLAG_PROFILE. */
+#define RG_K_EMBED      0
+#define RG_K_RMSNORM    1
+#define RG_K_GEMM_QKV   2
+#define RG_K_QKV_ROPE   3
+#define RG_K_ATTN       4
+#define RG_K_ATTN_MERGE 5
+#define RG_K_GEMM_O     6
+#define RG_K_GEMM_GU    7
+#define RG_K_SWIGLU     8
+#define RG_K_GEMM_DOWN  9
+#define RG_K_RESIDUAL  10
+#define RG_K_GEMM_LM   11
+#define RG_K_SAMPLE    12
+#define RG_K_COMPACT   13
+#define RG_K_SETUP     14
+#define RG_K_COUNT     15
+/* Totals for kernel class `kind` over the decode steps (phase 1) or the
+ * prefill (phase 0) of the last profiled rollout: summed launch durations in
+ * milliseconds (HIP events) and the number of launches. */
+int rg_kernel_times(const rg_policy* pol, int32_t phase, int32_t kind, double* total_ms,
+                    int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PAPER_2606_02218_ROLLOUT_H */

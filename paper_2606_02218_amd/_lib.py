@@ -1,0 +1,249 @@
+"""ctypes marshalling for include/rollout.h.  No computation happens here."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "librollout.so")
+_lib = None
+
+RG_OK, RG_EINVAL, RG_ENOMEM, RG_EHIP, RG_EUNSUPPORTED = 0, -1, -2, -3, -4
+RG_DTYPE_F32, RG_DTYPE_BF16 = 0, 1
+RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE = 1, 2
+KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge", "gemm_o", "gemm_gu", "swiglu",
+                "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup"]
+
+EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
+           "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times"]
+
+
+class RolloutError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class rg_config(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32), ("vocab", C.c_int32),
+                ("eos_id", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("dtype", C.c_int32)]
+
+
+_PP = C.POINTER(C.c_void_p)
+
+
+class rg_weights(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
+                ("attn_norm", _PP), ("wq", _PP), ("wk", _PP), ("wv", _PP), ("wo", _PP), ("ffn_norm", _PP),
+                ("w_gate", _PP), ("w_up", _PP), ("w_down", _PP)]
+
+
+class rg_limits(C.Structure):
+    _fields_ = [("max_seqs", C.c_int32), ("max_prompts", C.c_int32), ("max_prompt_tokens", C.c_int32),
+                ("max_context", C.c_int32), ("kv_pool_pages", C.c_int64)]
+
+
+class rg_sampling(C.Structure):
+    _fields_ = [("temperature", C.c_float), ("flags", C.c_int32), ("forced_len", C.POINTER(C.c_int32)),
+                ("force_tokens", C.c_void_p), ("dump_logits", C.c_void_p), ("dump_steps", C.c_int32)]
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load librollout.so; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2606_02218_amd.build` "
+                          "(or __graft_entry__.build()); there is no fallback path")
+    lib = C.CDLL(_LIB_PATH)
+    lib.rg_last_error.restype = C.c_char_p
+    lib.rg_policy_create.argtypes = [C.POINTER(rg_config), C.POINTER(rg_weights), C.POINTER(rg_limits),
+                                     C.POINTER(C.c_void_p)]
+    lib.rg_policy_destroy.argtypes = [C.c_void_p]
+    lib.rg_policy_destroy.restype = None
+    lib.rg_policy_device_bytes.argtypes = [C.c_void_p]
+    lib.rg_policy_device_bytes.restype = C.c_int64
+    lib.rollout_group.argtypes = [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32),
+                                  C.c_int32, C.c_uint64, C.POINTER(rg_sampling), C.c_void_p, C.c_void_p, C.c_void_p,
+                                  C.c_void_p]
+    lib.group_advantage.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_int32, C.c_void_p,
+                                    C.c_void_p]
+    lib.rg_philox_blocks.argtypes = [C.c_uint64, C.c_uint64, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
+    lib.rg_gumbel_bits.argtypes = [C.c_uint64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    lib.rg_step_history.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_void_p, C.c_void_p, C.c_void_p]
+    lib.rg_kernel_times.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    _lib = lib
+    return lib
+
+
+def exported_symbols() -> list:
+    lib = load_library()
+    return [n for n in EXPORTS if hasattr(lib, n)]
+
+
+def _check(rc: int):
+    if rc != RG_OK:
+        raise RolloutError(rc, load_library().rg_last_error().decode())
+
+
+def _stream_ptr(stream=None) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+class Policy:
+    """A decoder loaded into librollout (the library copies the weights)."""
+
+    def __init__(self, shape, weights, max_seqs: int, max_prompts: int, max_prompt_tokens: int, max_context: int,
+                 kv_pool_pages: int = 0, device: str = "cuda"):
+        import torch
+        lib = load_library()
+        self.shape = shape
+        self.device = torch.device(device)
+        dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        cfg = rg_config(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                        shape.ffn_dim, shape.vocab, shape.eos_id, float(shape.rope_theta), float(shape.rms_eps),
+                        RG_DTYPE_BF16 if shape.dtype == "bf16" else RG_DTYPE_F32)
+        keep = []
+
+        def up(a, dtype):
+            t = torch.from_numpy(np.ascontiguousarray(a)).to(device=self.device).to(dtype)
+            keep.append(t)
+            return t.data_ptr()
+
+        def arr(name, dtype):
+            a = (C.c_void_p * shape.n_layers)(*[up(lw[name], dtype) for lw in weights.layers])
+            keep.append(a)
+            return C.cast(a, _PP)
+
+        w = rg_weights(up(weights.embed, dt), up(weights.final_norm, torch.float32), up(weights.lm_head, dt),
+                       arr("attn_norm", torch.float32), arr("wq", dt), arr("wk", dt), arr("wv", dt), arr("wo", dt),
+                       arr("ffn_norm", torch.float32), arr("w_gate", dt), arr("w_up", dt), arr("w_down", dt))
+        lim = rg_limits(max_seqs, max_prompts, max_prompt_tokens, max_context, kv_pool_pages)
+        h = C.c_void_p()
+        torch.cuda.synchronize()
+        _check(lib.rg_policy_create(C.byref(cfg), C.byref(w), C.byref(lim), C.byref(h)))
+        torch.cuda.synchronize()
+        del keep
+        self._h = h
+        self.limits = lim
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load_library().rg_policy_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def device_bytes(self) -> int:
+        return int(load_library().rg_policy_device_bytes(self._h))
+
+    def rollout(self, prompts, G: Sequence[int], max_new: int, seed: int, temperature: float = 1.0,
+                forced_len=None, force_tokens=None, dump_steps: int = 0, share_prefix: bool = True,
+                profile: bool = False, out=None, stream=None):
+        """prompts: device int32 tensor [P, Lp] or a list of 1-D device int32
+        tensors.  Returns (tokens [N, max_new], lengths [N], logprobs
+        [N, max_new]) and, with dump_steps, the logits [dump_steps, N, V]."""
+        import torch
+        lib = load_library()
+        if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
+            plen = [prompts.shape[1]] * prompts.shape[0]
+            packed = prompts.contiguous().view(-1)
+        else:
+            plen = [int(p.numel()) for p in prompts]
+            packed = torch.cat([p.view(-1) for p in prompts])
+        if packed.dtype != torch.int32 or packed.device.type != "cuda":
+            raise TypeError("prompts must be int32 tensors on the GPU")
+        P = len(plen)
+        G = [int(g) for g in G]
+        N = sum(G)
+        dev = packed.device
+        if out is None:
+            tokens = torch.empty((N, max_new), dtype=torch.int32, device=dev)
+            lengths = torch.empty(N, dtype=torch.int32, device=dev)
+            logprobs = torch.empty((N, max_new), dtype=torch.float32, device=dev)
+        else:
+            tokens, lengths, logprobs = out
+        dump = torch.empty((dump_steps, N, self.shape.vocab), dtype=torch.float32, device=dev) if dump_steps else None
+        flags = (0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+        fl = None
+        if forced_len is not None:
+            fl_np = np.ascontiguousarray(np.asarray(forced_len, dtype=np.int32))
+            fl = fl_np.ctypes.data_as(C.POINTER(C.c_int32))
+        ft = None
+        if force_tokens is not None:
+            ft = force_tokens.to(device=dev, dtype=torch.int32).contiguous()
+        opts = rg_sampling(float(temperature), flags, fl, _ptr(ft), _ptr(dump), dump_steps)
+        plen_a = (C.c_int32 * P)(*plen)
+        g_a = (C.c_int32 * P)(*G)
+        _check(lib.rollout_group(self._h, _ptr(packed), plen_a, P, g_a, max_new, C.c_uint64(seed & (2 ** 64 - 1)),
+                                 C.byref(opts), _ptr(tokens), _ptr(lengths), _ptr(logprobs), _stream_ptr(stream)))
+        if dump_steps:
+            return tokens, lengths, logprobs, dump
+        return tokens, lengths, logprobs
+
+    def step_history(self, cap: int = 1 << 16):
+        lib = load_library()
+        n = C.c_int32()
+        a = np.zeros(cap, np.int32); g = np.zeros(cap, np.int32); c = np.zeros(cap, np.int64)
+        _check(lib.rg_step_history(self._h, cap, C.byref(n), a.ctypes.data, g.ctypes.data, c.ctypes.data))
+        k = min(cap, n.value)
+        return a[:k].copy(), g[:k].copy(), c[:k].copy()
+
+    def kernel_times(self, phase: int = 1) -> dict:
+        lib = load_library()
+        out = {}
+        for i, name in enumerate(KERNEL_KINDS):
+            ms = C.c_double(); n = C.c_int64()
+            _check(lib.rg_kernel_times(self._h, phase, i, C.byref(ms), C.byref(n)))
+            out[name] = (ms.value, n.value)
+        return out
+
+
+def group_advantage(rewards, G_dev, eps: float = 1e-6, ddof: int = 1, out=None, stream=None):
+    """rewards: device fp32 [N]; G_dev: device int32 [P]."""
+    import torch
+    lib = load_library()
+    if out is None:
+        out = torch.empty_like(rewards)
+    _check(lib.group_advantage(_ptr(rewards), _ptr(G_dev), int(G_dev.numel()), int(rewards.numel()), float(eps),
+                               int(ddof), _ptr(out), _stream_ptr(stream)))
+    return out
+
+
+def philox_blocks(key0: int, key1: int, ctr, stream=None):
+    """ctr: device int64/uint64 tensor [n, 4] (bit patterns); returns [n, 4]."""
+    import torch
+    lib = load_library()
+    ctr = ctr.contiguous()
+    out = torch.empty_like(ctr)
+    _check(lib.rg_philox_blocks(C.c_uint64(key0), C.c_uint64(key1), _ptr(ctr), ctr.shape[0], _ptr(out),
+                                _stream_ptr(stream)))
+    return out
+
+
+def gumbel_bits(seed: int, t: int, s: int, vocab: int, stream=None):
+    """Returns a device int32 tensor [vocab] holding the uint32 bit patterns."""
+    import torch
+    lib = load_library()
+    out = torch.empty(vocab, dtype=torch.int32, device="cuda")
+    _check(lib.rg_gumbel_bits(C.c_uint64(seed), t, s, vocab, _ptr(out), _stream_ptr(stream)))
+    return out

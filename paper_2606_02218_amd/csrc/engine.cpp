@@ -1,0 +1,659 @@
+// Host side of librollout.so: policy creation (weight repacking, workspace
+// arena, KV page pool), the rollout driver and the C ABI declared in
+// include/rollout.h.
+//
+// Rollout driver.  Prefill runs every prompt once over all prompt tokens as
+// one batch of rows, writing keys/values into the prompt's KV pages; the lm
+// head runs on each prompt's last position.  The fork gives every sibling the
+// prompt's full pages by reference.  Step 0 samples every sibling from its
+// prompt's logits; step t >= 1 feeds each active sequence's previous token
+// through the decoder.  After each step one kernel retires finished rows and
+// compacts the survivors; the active count is copied back asynchronously and
+// the host sizes later grids with the last count it has seen (an upper bound,
+// since the count never grows), running at most RG_LOOKAHEAD steps ahead.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "rollout.h"
+#include "rg_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIPTRY(expr)                                                                         \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(RG_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
+constexpr int RG_SPLIT_MAX = 16;       // largest split-K factor of a decode GEMM
+constexpr int RG_GEMM_TARGET = 1024;   // blocks a GEMM launch aims for
+constexpr int RG_ATT_TARGET = 1024;    // blocks an attention launch aims for
+constexpr int RG_RING = 64;            // async active-count slots
+constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
+constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+struct rg_policy {
+  rg_config cfg{};
+  rg_limits lim{};
+  int dtype = 0;
+  size_t eb = 4;
+  int d = 0, V = 0, L = 0, F = 0, hd = 0, nq = 0, nkv = 0, q_dim = 0, kv_dim = 0, qkv_n = 0;
+  int page_tok = RG_PAGE_TOK, max_pages = 0, m_act = 0;
+  KvGeom geom{};
+
+  void* w_embed = nullptr;
+  float* w_final = nullptr;
+  void* w_lm = nullptr;
+  std::vector<void*> w_qkv, w_o, w_gu, w_down;
+  std::vector<float*> g_attn, g_ffn;
+  float* rope_cos = nullptr;
+  float* rope_sin = nullptr;
+
+  void* kv_pool = nullptr;
+  int64_t pool_pages = 0;
+
+  float* x = nullptr;
+  void* abuf = nullptr;
+  int64_t a_plane = 0;   // elements between the hi and lo planes of abuf (bf16 models)
+  float* cpart = nullptr;
+  int64_t cpart_elems = 0;
+  float* qbuf = nullptr;
+  float* att_o = nullptr;
+  float* att_ml = nullptr;
+  int64_t att_rowchunks = 0;
+  float* logits = nullptr;
+  int32_t *page_tab = nullptr, *seq_grp = nullptr, *seq_npages = nullptr, *seq_nshared = nullptr,
+          *seq_forced = nullptr, *grp_off = nullptr, *prompt_off = nullptr, *plen = nullptr, *G_dev = nullptr,
+          *act_seq = nullptr, *act_tok = nullptr, *done = nullptr, *row_tab = nullptr, *row_pos = nullptr,
+          *free_stack = nullptr, *state = nullptr, *copy_pairs = nullptr, *last_rows = nullptr,
+          *hist_active = nullptr, *hist_groups = nullptr;
+  int64_t* hist_ctx = nullptr;
+  int hist_cap = 0;
+
+  int32_t* h_stage = nullptr;  // pinned staging for host inputs
+  int32_t* h_ring = nullptr;   // pinned [RG_RING][8] state snapshots
+  hipEvent_t ring_ev[RG_RING]{};
+
+  std::vector<void*> allocs;
+  int64_t dev_bytes = 0;
+
+  // profiling
+  bool prof = false;
+  int prof_phase = 0;
+  std::vector<hipEvent_t> prof_ev;  // 2 * RG_PROF_RING
+  std::vector<int> prof_kind, prof_ph;
+  int64_t prof_head = 0, prof_tail = 0;
+  double kt_ms[2][RG_K_COUNT]{};
+  int64_t kt_n[2][RG_K_COUNT]{};
+
+  int32_t last_steps = 0;
+
+  int alloc(void** p, size_t bytes) {
+    bytes = std::max<size_t>(bytes, 256);
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? RG_ENOMEM : RG_EHIP,
+                                     "hipMalloc(" + std::to_string(bytes) + "): " + hipGetErrorString(e));
+    allocs.push_back(*p);
+    dev_bytes += (int64_t)bytes;
+    return RG_OK;
+  }
+  ~rg_policy() {
+    for (void* p : allocs) (void)hipFree(p);
+    if (h_stage) (void)hipHostFree(h_stage);
+    if (h_ring) (void)hipHostFree(h_ring);
+    for (auto& e : ring_ev) if (e) (void)hipEventDestroy(e);
+    for (auto& e : prof_ev) if (e) (void)hipEventDestroy(e);
+  }
+};
+
+namespace {
+
+// ---------------------------------------------------------------- profiling
+int prof_drain_one(rg_policy* p) {
+  const int64_t i = p->prof_tail % RG_PROF_RING;
+  HIPTRY(hipEventSynchronize(p->prof_ev[2 * i + 1]));
+  float ms = 0.f;
+  HIPTRY(hipEventElapsedTime(&ms, p->prof_ev[2 * i], p->prof_ev[2 * i + 1]));
+  p->kt_ms[p->prof_ph[i]][p->prof_kind[i]] += ms;
+  p->kt_n[p->prof_ph[i]][p->prof_kind[i]] += 1;
+  p->prof_tail++;
+  return RG_OK;
+}
+
+struct ProfScope {
+  rg_policy* p;
+  hipStream_t st;
+  int64_t slot = -1;
+  int rc = RG_OK;
+  ProfScope(rg_policy* pol, hipStream_t s, int kind) : p(pol), st(s) {
+    if (!p->prof) return;
+    if (p->prof_head - p->prof_tail >= RG_PROF_RING) rc = prof_drain_one(p);
+    slot = p->prof_head % RG_PROF_RING;
+    p->prof_kind[slot] = kind;
+    p->prof_ph[slot] = p->prof_phase;
+    (void)hipEventRecord(p->prof_ev[2 * slot], st);
+  }
+  ~ProfScope() {
+    if (slot < 0) return;
+    (void)hipEventRecord(p->prof_ev[2 * slot + 1], st);
+    p->prof_head++;
+  }
+};
+
+#define LAUNCH(kind, call)                                                                    \
+  do {                                                                                        \
+    ProfScope ps_(pol, st, kind);                                                             \
+    if (ps_.rc != RG_OK) return ps_.rc;                                                        \
+    hipError_t e_ = (call);                                                                   \
+    if (e_ != hipSuccess) return fail(RG_EHIP, std::string("launch ") + #kind + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits, int* kps) {
+  int S = 1;
+  if (pol->dtype == RG_DTYPE_BF16) {
+    const int64_t blocks = ceil_div(N, 64) * ceil_div(rows_ub, 64);
+    if (blocks < RG_GEMM_TARGET) S = (int)std::min<int64_t>(ceil_div(RG_GEMM_TARGET, blocks), K / 256);
+    S = std::max(1, std::min(S, RG_SPLIT_MAX));
+  }
+  int k = (int)ceil_div(ceil_div(K, S), 32) * 32;
+  *kps = k;
+  *splits = (int)ceil_div(K, k);
+}
+
+int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const void* W, int N, float* C,
+         const int* d_rows, int rows_ub, int* splits_out, int64_t* stride_out) {
+  int S, kps;
+  if (C == pol->cpart) {
+    choose_splits(pol, N, rows_ub, K, &S, &kps);
+    const int64_t fit = pol->cpart_elems / ((int64_t)rows_ub * N);   // splits the workspace holds
+    if (S > fit) {
+      S = (int)std::max<int64_t>(1, fit);
+      kps = (int)ceil_div(ceil_div(K, S), 32) * 32;
+      S = (int)ceil_div(K, kps);
+    }
+  } else {   // direct output (the lm head into the logits buffer): never split
+    S = 1;
+    kps = K;
+  }
+  const int64_t stride = (int64_t)rows_ub * N;
+  if (C == pol->cpart && stride * S > pol->cpart_elems)
+    return fail(RG_ENOMEM, "GEMM workspace too small");
+  LAUNCH(kind, launch_gemm(pol->dtype, A, K, pol->a_plane, W, K, C, N, stride, d_rows, rows_ub, N, K, S, kps, st));
+  if (splits_out) *splits_out = S;
+  if (stride_out) *stride_out = stride;
+  return RG_OK;
+}
+
+// The decoder blocks over `rows_ub` rows (actual count at *d_rows), whose
+// row_tab / row_pos are set; ctx_max bounds every row's context length.
+int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max) {
+  if (rows_ub <= 0) return RG_OK;
+  const int tab_stride = pol->max_pages;
+  int n_chunks = 1;
+  if ((int64_t)rows_ub * pol->nkv < RG_ATT_TARGET)
+    n_chunks = (int)std::min<int64_t>(ceil_div(RG_ATT_TARGET, (int64_t)rows_ub * pol->nkv), ceil_div(ctx_max, 256));
+  n_chunks = std::max(1, n_chunks);
+  const int chunk_len = (int)ceil_div(ceil_div(ctx_max, n_chunks), 64) * 64;
+  n_chunks = (int)ceil_div(ctx_max, chunk_len);
+  if ((int64_t)rows_ub * n_chunks > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
+
+  for (int l = 0; l < pol->L; ++l) {
+    int S;
+    int64_t stride;
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[l], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                         pol->a_plane, nullptr, d_rows, rows_ub, st));
+    int rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, pol->cpart, d_rows, rows_ub,
+                  &S, &stride);
+    if (rc) return rc;
+    LAUNCH(RG_K_QKV_ROPE, launch_qkv_rope(pol->dtype, pol->cpart, stride, S, pol->nq, pol->nkv, pol->hd,
+                                          pol->rope_cos, pol->rope_sin, pol->qbuf, pol->kv_pool, pol->geom, l,
+                                          pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, d_rows, rows_ub,
+                                          st));
+    LAUNCH(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
+                                       pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, chunk_len, n_chunks,
+                                       pol->att_o, pol->att_ml, d_rows, rows_ub, st));
+    LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
+                                              chunk_len, n_chunks, pol->abuf, pol->a_plane, d_rows, rows_ub, st));
+    rc = gemm(pol, st, RG_K_GEMM_O, pol->abuf, pol->q_dim, pol->w_o[l], pol->d, pol->cpart, d_rows, rows_ub, &S,
+              &stride);
+    if (rc) return rc;
+    LAUNCH(RG_K_RESIDUAL, launch_residual(pol->cpart, stride, S, pol->d, pol->x, d_rows, rows_ub, st));
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_ffn[l], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                         pol->a_plane, nullptr, d_rows, rows_ub, st));
+    rc = gemm(pol, st, RG_K_GEMM_GU, pol->abuf, pol->d, pol->w_gu[l], 2 * pol->F, pol->cpart, d_rows, rows_ub, &S,
+              &stride);
+    if (rc) return rc;
+    LAUNCH(RG_K_SWIGLU, launch_swiglu(pol->dtype, pol->cpart, stride, S, pol->F, pol->abuf, pol->a_plane, d_rows, rows_ub, st));
+    rc = gemm(pol, st, RG_K_GEMM_DOWN, pol->abuf, pol->F, pol->w_down[l], pol->d, pol->cpart, d_rows, rows_ub, &S,
+              &stride);
+    if (rc) return rc;
+    LAUNCH(RG_K_RESIDUAL, launch_residual(pol->cpart, stride, S, pol->d, pol->x, d_rows, rows_ub, st));
+  }
+  return RG_OK;
+}
+
+// Final norm + lm head for `rows_ub` rows into pol->logits.
+int run_head(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, const int32_t* src_rows) {
+  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->w_final, pol->d, pol->cfg.rms_eps, pol->abuf,
+                                       pol->a_plane, src_rows, d_rows, rows_ub, st));
+  return gemm(pol, st, RG_K_GEMM_LM, pol->abuf, pol->d, pol->w_lm, pol->V, pol->logits, d_rows, rows_ub, nullptr,
+              nullptr);
+}
+
+int copy_weight(rg_policy* pol, void* dst, const void* src, size_t bytes, const char* what) {
+  if (!src) return fail(RG_EINVAL, std::string("weights: NULL ") + what);
+  HIPTRY(hipMemcpy(dst, src, bytes, hipMemcpyDeviceToDevice));
+  return RG_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+const char* rg_last_error(void) { return g_err.c_str(); }
+
+int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits* limits, rg_policy** out) {
+  if (!cfg || !w || !limits || !out) return fail(RG_EINVAL, "rg_policy_create: NULL argument");
+  *out = nullptr;
+  const rg_config c = *cfg;
+  if (c.n_layers < 1 || c.d_model < 1 || c.n_q_heads < 1 || c.n_kv_heads < 1 || c.head_dim < 2 || c.ffn_dim < 1 ||
+      c.vocab < 2 || c.eos_id < 0 || c.eos_id >= c.vocab || !(c.rope_theta > 0.f) || !(c.rms_eps >= 0.f))
+    return fail(RG_EINVAL, "rg_policy_create: invalid config");
+  if (c.dtype != RG_DTYPE_F32 && c.dtype != RG_DTYPE_BF16) return fail(RG_EUNSUPPORTED, "unsupported dtype");
+  if (c.head_dim % 8 || c.head_dim > 256 || c.n_q_heads % c.n_kv_heads || c.n_q_heads / c.n_kv_heads > 8 ||
+      c.d_model % 32 || (c.n_q_heads * c.head_dim) % 32 || c.ffn_dim % 32 || c.vocab % 16)
+    return fail(RG_EUNSUPPORTED, "unsupported shape: need head_dim%8==0, head_dim<=256, n_q/n_kv integer <= 8, "
+                                 "d_model, n_q*head_dim, ffn_dim multiples of 32, vocab multiple of 16");
+  const rg_limits lim = *limits;
+  if (lim.max_seqs < 1 || lim.max_prompts < 1 || lim.max_prompt_tokens < 1 || lim.max_context < 2 ||
+      lim.kv_pool_pages < 0)
+    return fail(RG_EINVAL, "rg_policy_create: invalid limits");
+
+  rg_policy* pol = new rg_policy();
+  auto bail = [&](int rc) { delete pol; return rc; };
+  pol->cfg = c;
+  pol->lim = lim;
+  pol->dtype = c.dtype;
+  pol->eb = c.dtype == RG_DTYPE_BF16 ? 2 : 4;
+  pol->d = c.d_model; pol->V = c.vocab; pol->L = c.n_layers; pol->F = c.ffn_dim; pol->hd = c.head_dim;
+  pol->nq = c.n_q_heads; pol->nkv = c.n_kv_heads;
+  pol->q_dim = c.n_q_heads * c.head_dim;
+  pol->kv_dim = c.n_kv_heads * c.head_dim;
+  pol->qkv_n = pol->q_dim + 2 * pol->kv_dim;
+  pol->max_pages = (int)ceil_div(lim.max_context, pol->page_tok) + 1;
+  pol->m_act = std::max(lim.max_prompt_tokens, lim.max_seqs);
+  KvGeom& g = pol->geom;
+  g.page_tok = pol->page_tok; g.n_layers = pol->L; g.n_kv = pol->nkv; g.head_dim = pol->hd;
+  g.layer_elems = 2LL * pol->nkv * pol->page_tok * pol->hd;
+  g.page_elems = g.layer_elems * pol->L;
+  const size_t eb = pol->eb;
+  const int64_t d = pol->d;
+  int rc;
+
+  // ---- weights (repacked: [wq; wk; wv] and [w_gate; w_up] stacked by rows)
+  if ((rc = pol->alloc(&pol->w_embed, (size_t)pol->V * d * eb))) return bail(rc);
+  if ((rc = copy_weight(pol, pol->w_embed, w->embed, (size_t)pol->V * d * eb, "embed"))) return bail(rc);
+  if ((rc = pol->alloc(&pol->w_lm, (size_t)pol->V * d * eb))) return bail(rc);
+  if ((rc = copy_weight(pol, pol->w_lm, w->lm_head, (size_t)pol->V * d * eb, "lm_head"))) return bail(rc);
+  if ((rc = pol->alloc((void**)&pol->w_final, d * 4))) return bail(rc);
+  if ((rc = copy_weight(pol, pol->w_final, w->final_norm, d * 4, "final_norm"))) return bail(rc);
+  if (!w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo || !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return bail(fail(RG_EINVAL, "weights: NULL per-layer array"));
+  for (int l = 0; l < pol->L; ++l) {
+    void *qkv, *o, *gu, *dn;
+    float *ga, *gf;
+    if ((rc = pol->alloc(&qkv, (size_t)pol->qkv_n * d * eb))) return bail(rc);
+    char* q = (char*)qkv;
+    if ((rc = copy_weight(pol, q, w->wq[l], (size_t)pol->q_dim * d * eb, "wq"))) return bail(rc);
+    if ((rc = copy_weight(pol, q + (size_t)pol->q_dim * d * eb, w->wk[l], (size_t)pol->kv_dim * d * eb, "wk"))) return bail(rc);
+    if ((rc = copy_weight(pol, q + (size_t)(pol->q_dim + pol->kv_dim) * d * eb, w->wv[l], (size_t)pol->kv_dim * d * eb, "wv")))
+      return bail(rc);
+    if ((rc = pol->alloc(&o, (size_t)d * pol->q_dim * eb))) return bail(rc);
+    if ((rc = copy_weight(pol, o, w->wo[l], (size_t)d * pol->q_dim * eb, "wo"))) return bail(rc);
+    if ((rc = pol->alloc(&gu, (size_t)2 * pol->F * d * eb))) return bail(rc);
+    if ((rc = copy_weight(pol, gu, w->w_gate[l], (size_t)pol->F * d * eb, "w_gate"))) return bail(rc);
+    if ((rc = copy_weight(pol, (char*)gu + (size_t)pol->F * d * eb, w->w_up[l], (size_t)pol->F * d * eb, "w_up"))) return bail(rc);
+    if ((rc = pol->alloc(&dn, (size_t)d * pol->F * eb))) return bail(rc);
+    if ((rc = copy_weight(pol, dn, w->w_down[l], (size_t)d * pol->F * eb, "w_down"))) return bail(rc);
+    if ((rc = pol->alloc((void**)&ga, d * 4))) return bail(rc);
+    if ((rc = copy_weight(pol, ga, w->attn_norm[l], d * 4, "attn_norm"))) return bail(rc);
+    if ((rc = pol->alloc((void**)&gf, d * 4))) return bail(rc);
+    if ((rc = copy_weight(pol, gf, w->ffn_norm[l], d * 4, "ffn_norm"))) return bail(rc);
+    pol->w_qkv.push_back(qkv); pol->w_o.push_back(o); pol->w_gu.push_back(gu); pol->w_down.push_back(dn);
+    pol->g_attn.push_back(ga); pol->g_ffn.push_back(gf);
+  }
+
+  // ---- RoPE table: angle pos * theta^(-2i/hd) in double, stored as fp32 cos/sin
+  {
+    const int half = pol->hd / 2;
+    const size_t n = (size_t)lim.max_context * half;
+    std::vector<float> cs(n), sn(n);
+    for (int i = 0; i < half; ++i) {
+      const double inv = std::pow((double)c.rope_theta, -2.0 * i / (double)pol->hd);
+      for (int p = 0; p < lim.max_context; ++p) {
+        const double a = (double)p * inv;
+        cs[(size_t)p * half + i] = (float)std::cos(a);
+        sn[(size_t)p * half + i] = (float)std::sin(a);
+      }
+    }
+    if ((rc = pol->alloc((void**)&pol->rope_cos, n * 4))) return bail(rc);
+    if ((rc = pol->alloc((void**)&pol->rope_sin, n * 4))) return bail(rc);
+    HIPTRY(hipMemcpy(pol->rope_cos, cs.data(), n * 4, hipMemcpyHostToDevice));
+    HIPTRY(hipMemcpy(pol->rope_sin, sn.data(), n * 4, hipMemcpyHostToDevice));
+  }
+
+  // ---- KV page pool
+  pol->pool_pages = lim.kv_pool_pages;
+  if (pol->pool_pages == 0)
+    pol->pool_pages = ceil_div(lim.max_prompt_tokens, pol->page_tok) + lim.max_prompts +
+                      (int64_t)lim.max_seqs * (ceil_div(lim.max_context, pol->page_tok) + 1);
+  if (pol->pool_pages > INT32_MAX) return bail(fail(RG_ENOMEM, "KV pool exceeds 2^31 pages"));
+  if ((rc = pol->alloc(&pol->kv_pool, (size_t)pol->pool_pages * g.page_elems * eb))) return bail(rc);
+
+  // ---- workspace
+  const int64_t M = pol->m_act, S = lim.max_seqs, P = lim.max_prompts;
+  const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
+  pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
+  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + RG_ATT_TARGET;
+  pol->hist_cap = lim.max_context;
+  struct Piece { void** p; size_t bytes; };
+  const int64_t kmax = std::max<int64_t>({d, pol->q_dim, pol->F});
+  pol->a_plane = pol->dtype == RG_DTYPE_BF16 ? M * kmax : 0;
+  std::vector<Piece> pieces = {
+      {(void**)&pol->x, (size_t)(M * d * 4)},
+      {&pol->abuf, (size_t)(M * kmax * 4)},   // fp32, or two bf16 planes
+      {(void**)&pol->cpart, (size_t)(pol->cpart_elems * 4)},
+      {(void**)&pol->qbuf, (size_t)(M * pol->q_dim * 4)},
+      {(void**)&pol->att_o, (size_t)(pol->att_rowchunks * pol->nq * pol->hd * 4)},
+      {(void**)&pol->att_ml, (size_t)(pol->att_rowchunks * pol->nq * 2 * 4)},
+      {(void**)&pol->logits, (size_t)(std::max(S, P) * pol->V * 4)},
+      {(void**)&pol->page_tab, (size_t)((S + P) * pol->max_pages * 4)},
+      {(void**)&pol->seq_grp, (size_t)(S * 4)},
+      {(void**)&pol->seq_npages, (size_t)(S * 4)},
+      {(void**)&pol->seq_nshared, (size_t)(S * 4)},
+      {(void**)&pol->seq_forced, (size_t)(S * 4)},
+      {(void**)&pol->grp_off, (size_t)((P + 1) * 4)},
+      {(void**)&pol->prompt_off, (size_t)((P + 1) * 4)},
+      {(void**)&pol->plen, (size_t)(P * 4)},
+      {(void**)&pol->G_dev, (size_t)(P * 4)},
+      {(void**)&pol->last_rows, (size_t)(P * 4)},
+      {(void**)&pol->act_seq, (size_t)(S * 4)},
+      {(void**)&pol->act_tok, (size_t)(S * 4)},
+      {(void**)&pol->done, (size_t)(S * 4)},
+      {(void**)&pol->row_tab, (size_t)(M * 4)},
+      {(void**)&pol->row_pos, (size_t)(M * 4)},
+      {(void**)&pol->free_stack, (size_t)(pol->pool_pages * 4)},
+      {(void**)&pol->state, 64},
+      {(void**)&pol->copy_pairs, (size_t)(2 * S * pol->max_pages * 4)},
+      {(void**)&pol->hist_active, (size_t)(pol->hist_cap * 4)},
+      {(void**)&pol->hist_groups, (size_t)(pol->hist_cap * 4)},
+      {(void**)&pol->hist_ctx, (size_t)(pol->hist_cap * 8)},
+  };
+  size_t total = 0;
+  for (auto& pc : pieces) total += (pc.bytes + 255) & ~(size_t)255;
+  char* arena;
+  if ((rc = pol->alloc((void**)&arena, total))) return bail(rc);
+  for (auto& pc : pieces) {
+    *pc.p = arena;
+    arena += (pc.bytes + 255) & ~(size_t)255;
+  }
+  {
+    hipError_t e = hipHostMalloc((void**)&pol->h_stage, (size_t)(2 * P + S + 64) * 4, hipHostMallocDefault);
+    if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipHostMalloc: ") + hipGetErrorString(e)));
+    e = hipHostMalloc((void**)&pol->h_ring, (size_t)RG_RING * 8 * 4, hipHostMallocDefault);
+    if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipHostMalloc: ") + hipGetErrorString(e)));
+    for (auto& ev : pol->ring_ev) {
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipEventCreate: ") + hipGetErrorString(e)));
+    }
+  }
+  *out = pol;
+  return RG_OK;
+}
+
+void rg_policy_destroy(rg_policy* pol) { delete pol; }
+
+int64_t rg_policy_device_bytes(const rg_policy* pol) { return pol ? pol->dev_bytes : 0; }
+
+int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_len, int32_t P, const int32_t* G,
+                  int32_t max_new, uint64_t seed, const rg_sampling* opts, int32_t* tokens, int32_t* lengths,
+                  float* logprobs, void* stream) {
+  if (!pol || !prompts || !prompt_len || !G || !tokens || !lengths || !logprobs)
+    return fail(RG_EINVAL, "rollout_group: NULL argument");
+  hipStream_t st = (hipStream_t)stream;
+  const rg_limits& lim = pol->lim;
+  if (P < 1) return fail(RG_EINVAL, "rollout_group: P < 1");
+  if (max_new < 1) return fail(RG_EINVAL, "rollout_group: max_new < 1");
+  if (P > lim.max_prompts) return fail(RG_ENOMEM, "rollout_group: P exceeds limits.max_prompts");
+  int64_t N = 0, T_pre = 0;
+  int max_plen = 0;
+  for (int p = 0; p < P; ++p) {
+    if (prompt_len[p] < 1) return fail(RG_EINVAL, "rollout_group: prompt_len < 1");
+    if (G[p] < 1) return fail(RG_EINVAL, "rollout_group: G < 1");
+    N += G[p];
+    T_pre += prompt_len[p];
+    max_plen = std::max(max_plen, prompt_len[p]);
+  }
+  if (N > lim.max_seqs) return fail(RG_ENOMEM, "rollout_group: sum(G) exceeds limits.max_seqs");
+  if (T_pre > lim.max_prompt_tokens) return fail(RG_ENOMEM, "rollout_group: prompt tokens exceed limits");
+  if ((int64_t)max_plen + max_new > lim.max_context) return fail(RG_ENOMEM, "rollout_group: context exceeds limits");
+  rg_sampling o{};
+  o.temperature = 1.f;
+  if (opts) o = *opts;
+  if (!(o.temperature > 0.f) || !std::isfinite(o.temperature)) return fail(RG_EINVAL, "rollout_group: temperature <= 0");
+  if (o.dump_steps < 0) return fail(RG_EINVAL, "rollout_group: dump_steps < 0");
+  if (o.forced_len)
+    for (int64_t s = 0; s < N; ++s)
+      if (o.forced_len[s] < 1 || o.forced_len[s] > max_new) return fail(RG_EINVAL, "rollout_group: forced_len out of [1, max_new]");
+  const int Ni = (int)N;
+  {
+    int64_t pre_pages = 0;
+    for (int p = 0; p < P; ++p) pre_pages += ceil_div(prompt_len[p], pol->page_tok);
+    if (pre_pages > pol->pool_pages) return fail(RG_ENOMEM, "rollout_group: prompt pages exceed the KV pool");
+  }
+
+  // profiling state
+  pol->prof = (o.flags & RG_FLAG_PROFILE) != 0;
+  if (pol->prof) {
+    if (pol->prof_ev.empty()) {
+      pol->prof_ev.resize(2 * RG_PROF_RING);
+      pol->prof_kind.resize(RG_PROF_RING);
+      pol->prof_ph.resize(RG_PROF_RING);
+      for (auto& e : pol->prof_ev) HIPTRY(hipEventCreate(&e));
+    }
+    std::memset(pol->kt_ms, 0, sizeof(pol->kt_ms));
+    std::memset(pol->kt_n, 0, sizeof(pol->kt_n));
+    pol->prof_head = pol->prof_tail = 0;
+  }
+  pol->prof_phase = 0;
+
+  // stage host inputs: plen [P], G [P], forced [N]
+  int32_t* hs = pol->h_stage;
+  HIPTRY(hipStreamSynchronize(st));   // the staging buffer may still feed an earlier call's copies
+  std::memcpy(hs, prompt_len, (size_t)P * 4);
+  std::memcpy(hs + P, G, (size_t)P * 4);
+  HIPTRY(hipMemcpyAsync(pol->plen, hs, (size_t)P * 4, hipMemcpyHostToDevice, st));
+  HIPTRY(hipMemcpyAsync(pol->G_dev, hs + P, (size_t)P * 4, hipMemcpyHostToDevice, st));
+  if (o.forced_len) {
+    std::memcpy(hs + 2 * P, o.forced_len, (size_t)N * 4);
+    HIPTRY(hipMemcpyAsync(pol->seq_forced, hs + 2 * P, (size_t)N * 4, hipMemcpyHostToDevice, st));
+  }
+  const int32_t* forced_dev = o.forced_len ? pol->seq_forced : nullptr;
+
+  // set-up: offsets, prompt page tables, free stack, output padding
+  SetupArgs sa{};
+  sa.P = P; sa.n_seq = Ni; sa.max_new = max_new; sa.page_tok = pol->page_tok; sa.max_pages = pol->max_pages;
+  sa.pool_pages = pol->pool_pages; sa.plen = pol->plen; sa.prompt_off = pol->prompt_off; sa.grp_off = pol->grp_off;
+  sa.G = pol->G_dev; sa.page_tab = pol->page_tab; sa.free_stack = pol->free_stack; sa.state = pol->state;
+  sa.tokens_out = tokens; sa.logprobs_out = logprobs; sa.last_rows = pol->last_rows;
+  LAUNCH(RG_K_SETUP, launch_setup(sa, st));
+
+  // ---- prefill
+  const int* d_pre = pol->state + 5;
+  LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, Ni, pol->row_tab, pol->row_pos, (int)T_pre, st));
+  LAUNCH(RG_K_EMBED, launch_embed(pol->dtype, pol->w_embed, pol->d, pol->V, prompts, pol->x, pol->state + 7, d_pre,
+                                  (int)T_pre, st));
+  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen);
+  if (rc) return rc;
+  rc = run_head(pol, st, pol->state + 6, P, pol->last_rows);
+  if (rc) return rc;
+
+  // ---- fork
+  ForkArgs fa{};
+  fa.P = P; fa.n_seq = Ni; fa.page_tok = pol->page_tok; fa.max_pages = pol->max_pages;
+  fa.share = (o.flags & RG_FLAG_NO_PREFIX_SHARING) ? 0 : 1;
+  fa.grp_off = pol->grp_off; fa.plen = pol->plen; fa.page_tab = pol->page_tab; fa.seq_grp = pol->seq_grp;
+  fa.seq_npages = pol->seq_npages; fa.seq_nshared = pol->seq_nshared; fa.act_seq = pol->act_seq;
+  fa.free_stack = pol->free_stack; fa.state = pol->state; fa.copy_pairs = pol->copy_pairs;
+  LAUNCH(RG_K_SETUP, launch_fork(fa, st));
+  int max_pairs = 0;
+  for (int p = 0; p < P; ++p) {
+    const int n_pref = (int)ceil_div(prompt_len[p], pol->page_tok);
+    const int need = fa.share ? (prompt_len[p] % pol->page_tok ? 1 : 0) : n_pref;
+    max_pairs += need * G[p];
+  }
+  LAUNCH(RG_K_SETUP, launch_page_copy(pol->dtype, pol->kv_pool, pol->geom.page_elems, pol->copy_pairs, max_pairs,
+                                      pol->state, st));
+
+  // ---- sampling / retirement of one step
+  SampleArgs sm{};
+  sm.V = pol->V; sm.eos = pol->cfg.eos_id; sm.max_new = max_new; sm.seed = seed; sm.temperature = o.temperature;
+  sm.act_seq = pol->act_seq; sm.seq_grp = pol->seq_grp; sm.forced_len = forced_dev; sm.force_tokens = o.force_tokens;
+  sm.dump_logits = o.dump_logits; sm.dump_steps = o.dump_steps; sm.n_seq = Ni; sm.tokens_out = tokens;
+  sm.logprobs_out = logprobs; sm.next_tok = pol->act_tok; sm.done = pol->done; sm.d_rows = pol->state;
+  sm.bad_token = pol->state + 7;
+  sm.logits = pol->logits;
+  CompactArgs ca{};
+  ca.max_new = max_new; ca.page_tok = pol->page_tok; ca.max_pages = pol->max_pages; ca.n_seq = Ni;
+  ca.act_seq = pol->act_seq; ca.act_tok = pol->act_tok; ca.done = pol->done; ca.seq_grp = pol->seq_grp;
+  ca.plen = pol->plen; ca.page_tab = pol->page_tab; ca.seq_npages = pol->seq_npages; ca.seq_nshared = pol->seq_nshared;
+  ca.free_stack = pol->free_stack; ca.state = pol->state; ca.lengths = lengths; ca.hist_active = pol->hist_active;
+  ca.hist_groups = pol->hist_groups; ca.hist_ctx = pol->hist_ctx; ca.hist_cap = pol->hist_cap;
+
+  auto snapshot = [&](int t) -> int {
+    const int slot = t % RG_RING;
+    HIPTRY(hipMemcpyAsync(pol->h_ring + 8 * slot, pol->state, 32, hipMemcpyDeviceToHost, st));
+    HIPTRY(hipEventRecord(pol->ring_ev[slot], st));
+    return RG_OK;
+  };
+
+  // step 0
+  pol->prof_phase = 1;
+  sm.t = 0; sm.logits_by_group = 1;
+  LAUNCH(RG_K_SAMPLE, launch_sample(sm, Ni, st));
+  ca.t = 0;
+  LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
+  if ((rc = snapshot(0))) return rc;
+  HIPTRY(hipEventSynchronize(pol->ring_ev[0]));
+  int known_t = 0, last_t = 0;
+  int m_ub = pol->h_ring[0];
+  bool oom = pol->h_ring[2] != 0;
+  int n_steps = m_ub == 0 ? 1 : 0;
+
+  sm.logits_by_group = 0;
+  for (int t = 1; t < max_new && n_steps == 0 && !oom; ++t) {
+    // refresh the upper bound from completed snapshots; never run too far ahead
+    while (known_t + 1 < t) {
+      const int nx = (known_t + 1) % RG_RING;
+      if (t - known_t > RG_LOOKAHEAD) HIPTRY(hipEventSynchronize(pol->ring_ev[nx]));
+      else if (hipEventQuery(pol->ring_ev[nx]) != hipSuccess) break;
+      ++known_t;
+      m_ub = pol->h_ring[8 * nx];
+      if (pol->h_ring[8 * nx + 2]) oom = true;
+      if (m_ub == 0) { n_steps = known_t + 1; break; }
+    }
+    if (n_steps || oom) break;
+    LAUNCH(RG_K_EMBED, launch_decode_rows(pol->dtype, pol->w_embed, pol->d, pol->act_seq, pol->act_tok, pol->seq_grp,
+                                          pol->plen, t, pol->row_tab, pol->row_pos, pol->x, pol->state, m_ub, st));
+    if ((rc = run_layers(pol, st, pol->state, m_ub, max_plen + t))) return rc;
+    if ((rc = run_head(pol, st, pol->state, m_ub, nullptr))) return rc;
+    sm.t = t;
+    LAUNCH(RG_K_SAMPLE, launch_sample(sm, m_ub, st));
+    ca.t = t;
+    LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
+    if ((rc = snapshot(t))) return rc;
+    last_t = t;
+  }
+  HIPTRY(hipStreamSynchronize(st));
+  // snapshots the loop has not read yet (at most RG_LOOKAHEAD of them)
+  for (int k = known_t + 1; k <= last_t; ++k) {
+    const int nx = k % RG_RING;
+    if (pol->h_ring[8 * nx + 2]) oom = true;
+    if (pol->h_ring[8 * nx] == 0 && n_steps == 0) n_steps = k + 1;
+  }
+  if (n_steps == 0) n_steps = last_t + 1;
+  const bool bad_token = pol->h_ring[8 * (last_t % RG_RING) + 7] != 0;
+  pol->last_steps = n_steps;
+  if (pol->prof)
+    while (pol->prof_tail < pol->prof_head)
+      if ((rc = prof_drain_one(pol))) return rc;
+  if (oom) return fail(RG_ENOMEM, "rollout_group: the KV page pool ran out");
+  if (bad_token) return fail(RG_EINVAL, "rollout_group: a prompt or forced token id is outside [0, vocab)");
+  return RG_OK;
+}
+
+int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N, float eps, int32_t ddof, float* adv,
+                    void* stream) {
+  if (!rewards || !G || !adv) return fail(RG_EINVAL, "group_advantage: NULL argument");
+  if (P < 1 || N < 1) return fail(RG_EINVAL, "group_advantage: P < 1 or N < 1");
+  if (!(eps >= 0.f)) return fail(RG_EINVAL, "group_advantage: eps < 0");
+  if (ddof != 0 && ddof != 1) return fail(RG_EINVAL, "group_advantage: ddof must be 0 or 1");
+  if ((const void*)rewards == (const void*)adv) return fail(RG_EINVAL, "group_advantage: adv aliases rewards");
+  hipError_t e = launch_group_advantage(rewards, G, P, N, eps, ddof, adv, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("group_advantage launch: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
+int rg_philox_blocks(uint64_t key0, uint64_t key1, const uint64_t* ctr, int64_t n, uint64_t* out, void* stream) {
+  if (!ctr || !out || n < 0) return fail(RG_EINVAL, "rg_philox_blocks: bad argument");
+  hipError_t e = launch_philox_blocks(key0, key1, ctr, n, out, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("rg_philox_blocks: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
+int rg_gumbel_bits(uint64_t seed, int32_t t, int32_t s, int32_t vocab, uint32_t* out, void* stream) {
+  if (!out || vocab < 1 || t < 0 || s < 0) return fail(RG_EINVAL, "rg_gumbel_bits: bad argument");
+  hipError_t e = launch_gumbel_bits(seed, t, s, vocab, out, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("rg_gumbel_bits: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
+int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t* active, int32_t* groups,
+                    int64_t* ctx) {
+  if (!pol || cap < 0) return fail(RG_EINVAL, "rg_step_history: bad argument");
+  if (n_steps) *n_steps = pol->last_steps;
+  const int n = std::min(cap, std::min(pol->last_steps, pol->hist_cap));
+  if (n <= 0) return RG_OK;
+  if (active) HIPTRY(hipMemcpy(active, pol->hist_active, (size_t)n * 4, hipMemcpyDeviceToHost));
+  if (groups) HIPTRY(hipMemcpy(groups, pol->hist_groups, (size_t)n * 4, hipMemcpyDeviceToHost));
+  if (ctx) HIPTRY(hipMemcpy(ctx, pol->hist_ctx, (size_t)n * 8, hipMemcpyDeviceToHost));
+  return RG_OK;
+}
+
+int rg_kernel_times(const rg_policy* pol, int32_t phase, int32_t kind, double* total_ms, int64_t* launches) {
+  if (!pol || phase < 0 || phase > 1 || kind < 0 || kind >= RG_K_COUNT) return fail(RG_EINVAL, "rg_kernel_times: bad argument");
+  if (total_ms) *total_ms = pol->kt_ms[phase][kind];
+  if (launches) *launches = pol->kt_n[phase][kind];
+  return RG_OK;
+}
+
+}  // extern "C"

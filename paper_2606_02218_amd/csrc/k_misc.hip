@@ -1,0 +1,302 @@
+// Row-wise kernels of the decoder step: embedding gather and row set-up,
+// RMSNorm, the fused QKV epilogue (split-K sum, RoPE, KV append), residual
+// add, SwiGLU, page copies, plus the Philox test hooks.
+#include "rg_device.h"
+#include "rg_kernels.h"
+
+namespace {
+
+template <typename T>
+__global__ void k_embed(const T* __restrict__ embed, int d, int V, const int32_t* __restrict__ tok,
+                        float* __restrict__ x, int32_t* __restrict__ bad_token, const int* __restrict__ d_rows) {
+  const int r = blockIdx.x;
+  if (r >= *d_rows) return;
+  int id = tok[r];
+  if (id < 0 || id >= V) {
+    if (threadIdx.x == 0) bad_token[0] = 1;
+    id = 0;
+  }
+  const T* e = embed + (int64_t)id * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ld_f32<T>(e + i);
+}
+
+template <typename T>
+__global__ void k_decode_rows(const T* __restrict__ embed, int d, const int32_t* __restrict__ act_seq,
+                              const int32_t* __restrict__ act_tok, const int32_t* __restrict__ seq_grp,
+                              const int32_t* __restrict__ plen, int t, int32_t* __restrict__ row_tab,
+                              int32_t* __restrict__ row_pos, float* __restrict__ x, const int* __restrict__ d_rows) {
+  const int r = blockIdx.x;
+  if (r >= *d_rows) return;
+  const int s = act_seq[r];
+  if (threadIdx.x == 0) {
+    row_tab[r] = s;
+    row_pos[r] = plen[seq_grp[s]] + t - 1;
+  }
+  const T* e = embed + (int64_t)act_tok[r] * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ld_f32<T>(e + i);
+}
+
+__global__ void k_prefill_rows(const int32_t* __restrict__ prompt_off, int P, int tab_base,
+                               int32_t* __restrict__ row_tab, int32_t* __restrict__ row_pos, int total) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= total) return;
+  int lo = 0, hi = P - 1;   // last p with prompt_off[p] <= r
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (prompt_off[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  row_tab[r] = tab_base + lo;
+  row_pos[r] = r - prompt_off[lo];
+}
+
+template <int SPLIT>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, const float* __restrict__ g, int d,
+                                                 float eps, ActOut out, const int32_t* __restrict__ src_rows,
+                                                 const int* __restrict__ d_rows) {
+  const int r = blockIdx.x;
+  if (r >= *d_rows) return;
+  __shared__ float red[16];
+  const float* xr = x + (int64_t)(src_rows ? src_rows[r] : r) * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) ss = fmaf(xr[i], xr[i], ss);
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) act_store<SPLIT>(out, (int64_t)r * d + i, xr[i] * inv * g[i]);
+}
+
+template <typename KV>
+__global__ __launch_bounds__(256) void k_qkv_rope(const float* __restrict__ C, int64_t split_stride, int splits,
+                                                  int n_q, int n_kv, int hd, const float* __restrict__ rope_cos,
+                                                  const float* __restrict__ rope_sin, float* __restrict__ q_out,
+                                                  KV* __restrict__ pool, KvGeom g, int layer,
+                                                  const int32_t* __restrict__ page_tab, int tab_stride,
+                                                  const int32_t* __restrict__ row_tab,
+                                                  const int32_t* __restrict__ row_pos,
+                                                  const int* __restrict__ d_rows) {
+  const int r = blockIdx.x;
+  if (r >= *d_rows) return;
+  const int half = hd / 2;
+  const int ncols = (n_q + 2 * n_kv) * hd;
+  const float* cr = C + (int64_t)r * ncols;
+  const int pos = row_pos[r];
+  const int page = page_tab[(int64_t)row_tab[r] * tab_stride + pos / g.page_tok];
+  const int slot = pos % g.page_tok;
+  KV* kbase = pool + (int64_t)page * g.page_elems + (int64_t)layer * g.layer_elems;
+  KV* vbase = kbase + (int64_t)n_kv * g.page_tok * hd;
+  const float* cs = rope_cos + (int64_t)pos * half;
+  const float* sn = rope_sin + (int64_t)pos * half;
+  // rotated pairs of q and k heads
+  const int n_pairs = (n_q + n_kv) * half;
+  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
+    const int head = p / half, i = p % half;
+    const int c = head * hd + i;
+    float a = 0.f, b = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      a += cr[s * split_stride + c];
+      b += cr[s * split_stride + c + half];
+    }
+    const float co = cs[i], si = sn[i];
+    const float ra = a * co - b * si, rb = b * co + a * si;
+    if (head < n_q) {
+      float* qo = q_out + ((int64_t)r * n_q + head) * hd;
+      qo[i] = ra;
+      qo[i + half] = rb;
+    } else {
+      KV* kp = kbase + ((int64_t)(head - n_q) * g.page_tok + slot) * hd;
+      st_from_f32<KV>(kp + i, ra);
+      st_from_f32<KV>(kp + i + half, rb);
+    }
+  }
+  // values
+  const int nv = n_kv * hd;
+  for (int e = threadIdx.x; e < nv; e += blockDim.x) {
+    const int c = (n_q + n_kv) * hd + e;
+    float v = 0.f;
+    for (int s = 0; s < splits; ++s) v += cr[s * split_stride + c];
+    const int h = e / hd, dd = e % hd;
+    st_from_f32<KV>(vbase + ((int64_t)h * g.page_tok + slot) * hd + dd, v);
+  }
+}
+
+__global__ void k_residual(const float* __restrict__ C, int64_t split_stride, int splits, int N, float* __restrict__ x,
+                           const int* __restrict__ d_rows) {
+  const int r = blockIdx.y;
+  if (r >= *d_rows) return;
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  const int64_t o = (int64_t)r * N + n;
+  float v = 0.f;
+  for (int s = 0; s < splits; ++s) v += C[s * split_stride + o];
+  x[o] += v;
+}
+
+template <int SPLIT>
+__global__ void k_swiglu(const float* __restrict__ C, int64_t split_stride, int splits, int F, ActOut out,
+                         const int* __restrict__ d_rows) {
+  const int r = blockIdx.y;
+  if (r >= *d_rows) return;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= F) return;
+  const int64_t o = (int64_t)r * 2 * F + j;
+  float gt = 0.f, up = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    gt += C[s * split_stride + o];
+    up += C[s * split_stride + o + F];
+  }
+  const float silu = gt / (1.0f + expf(-gt));
+  act_store<SPLIT>(out, (int64_t)r * F + j, silu * up);
+}
+
+template <typename KV>
+__global__ void k_page_copy(KV* __restrict__ pool, int64_t page_elems, const int32_t* __restrict__ pairs,
+                            const int32_t* __restrict__ state) {
+  const int k = blockIdx.y;
+  if (k >= state[3]) return;
+  const KV* src = pool + (int64_t)pairs[2 * k] * page_elems;
+  KV* dst = pool + (int64_t)pairs[2 * k + 1] * page_elems;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < page_elems; i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+__global__ void k_fill_i32(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+__global__ void k_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* __restrict__ ctr, int64_t n,
+                                uint64_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  rg_u64x4 c;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c.v[j] = ctr[4 * i + j];
+  rg_u64x4 o = rg_philox4x64_10(c, k0, k1);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) out[4 * i + j] = o.v[j];
+}
+
+__global__ void k_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* __restrict__ out) {
+  const int vb = blockIdx.x * blockDim.x + threadIdx.x;
+  if (vb * 8 >= vocab) return;
+  rg_u64x4 c;
+  c.v[0] = (uint64_t)vb; c.v[1] = (uint64_t)t; c.v[2] = (uint64_t)s; c.v[3] = 0;
+  rg_u64x4 w = rg_philox4x64_10(c, seed, RG_TAG_GUMBEL);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int v = vb * 8 + j;
+    if (v < vocab) out[v] = (uint32_t)(w.v[j >> 1] >> (32 * (j & 1)));
+  }
+}
+
+}  // namespace
+
+
+hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_t* tok, float* x, int32_t* bad_token,
+                        const int* d_rows, int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_embed<bf16_t>, dim3(rows_ub), dim3(256), 0, st, (const bf16_t*)embed, d, V, tok, x, bad_token,
+                       d_rows);
+  else
+    hipLaunchKernelGGL(k_embed<float>, dim3(rows_ub), dim3(256), 0, st, (const float*)embed, d, V, tok, x, bad_token,
+                       d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq, const int32_t* act_tok,
+                              const int32_t* seq_grp, const int32_t* plen, int t, int32_t* row_tab, int32_t* row_pos,
+                              float* x, const int* d_rows, int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_decode_rows<bf16_t>, dim3(rows_ub), dim3(256), 0, st, (const bf16_t*)embed, d, act_seq, act_tok,
+                       seq_grp, plen, t, row_tab, row_pos, x, d_rows);
+  else
+    hipLaunchKernelGGL(k_decode_rows<float>, dim3(rows_ub), dim3(256), 0, st, (const float*)embed, d, act_seq, act_tok,
+                       seq_grp, plen, t, row_tab, row_pos, x, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_rows(const int32_t* prompt_off, int P, int tab_base, int32_t* row_tab, int32_t* row_pos,
+                               int total, hipStream_t st) {
+  if (total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_prefill_rows, dim3((total + 255) / 256), dim3(256), 0, st, prompt_off, P, tab_base, row_tab,
+                     row_pos, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, float eps, void* out, int64_t a_plane,
+                          const int32_t* src_rows, const int* d_rows, int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  const ActOut o{out, a_plane};
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_rmsnorm<1>, dim3(rows_ub), dim3(256), 0, st, x, g, d, eps, o, src_rows, d_rows);
+  else
+    hipLaunchKernelGGL(k_rmsnorm<0>, dim3(rows_ub), dim3(256), 0, st, x, g, d, eps, o, src_rows, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_rope(int dtype, const float* C, int64_t split_stride, int splits, int n_q, int n_kv,
+                           int head_dim, const float* rope_cos, const float* rope_sin, float* q_out, void* kv_pool,
+                           KvGeom g, int layer, const int32_t* page_tab, int tab_stride, const int32_t* row_tab,
+                           const int32_t* row_pos, const int* d_rows, int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_qkv_rope<bf16_t>, dim3(rows_ub), dim3(256), 0, st, C, split_stride, splits, n_q, n_kv, head_dim,
+                       rope_cos, rope_sin, q_out, (bf16_t*)kv_pool, g, layer, page_tab, tab_stride, row_tab, row_pos,
+                       d_rows);
+  else
+    hipLaunchKernelGGL(k_qkv_rope<float>, dim3(rows_ub), dim3(256), 0, st, C, split_stride, splits, n_q, n_kv, head_dim,
+                       rope_cos, rope_sin, q_out, (float*)kv_pool, g, layer, page_tab, tab_stride, row_tab, row_pos,
+                       d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_residual(const float* C, int64_t split_stride, int splits, int N, float* x, const int* d_rows,
+                           int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_residual, dim3((N + 255) / 256, rows_ub), dim3(256), 0, st, C, split_stride, splits, N, x, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu(int dtype, const float* C, int64_t split_stride, int splits, int F, void* out,
+                         int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st) {
+  if (rows_ub <= 0) return hipSuccess;
+  dim3 grid((F + 255) / 256, rows_ub);
+  const ActOut o{out, a_plane};
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_swiglu<1>, grid, dim3(256), 0, st, C, split_stride, splits, F, o, d_rows);
+  else
+    hipLaunchKernelGGL(k_swiglu<0>, grid, dim3(256), 0, st, C, split_stride, splits, F, o, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs, int max_pairs,
+                            const int32_t* state, hipStream_t st) {
+  if (max_pairs <= 0) return hipSuccess;
+  dim3 grid(64, max_pairs);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_page_copy<bf16_t>, grid, dim3(256), 0, st, (bf16_t*)kv_pool, page_elems, copy_pairs, state);
+  else
+    hipLaunchKernelGGL(k_page_copy<float>, grid, dim3(256), 0, st, (float*)kv_pool, page_elems, copy_pairs, state);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,
+                                hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_philox_blocks, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, k0, k1, ctr, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* out, hipStream_t st) {
+  const int nb = (vocab + 7) / 8;
+  hipLaunchKernelGGL(k_gumbel_bits, dim3((nb + 255) / 256), dim3(256), 0, st, seed, t, s, vocab, out);
+  return hipGetLastError();
+}

@@ -1,0 +1,147 @@
+// Host-side launchers of the rollout kernels.  Every launcher enqueues on
+// `st` and returns the launch status.  Row counts that change during decoding
+// are read by the kernels from device memory (`d_rows`); the grids are sized
+// by a host upper bound `rows_ub` and surplus blocks exit at once.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+struct KvGeom {
+  int page_tok;        // tokens per page
+  int n_layers, n_kv, head_dim;
+  int64_t page_elems;  // elements of one page across all layers
+  int64_t layer_elems; // elements of one layer inside a page: 2 * n_kv * page_tok * head_dim
+  // K of (layer l, kv head h, slot j) at  page*page_elems + l*layer_elems + (h*page_tok + j)*head_dim
+  // V at the same offset + n_kv*page_tok*head_dim
+};
+
+// dtype: 0 = fp32 storage, 1 = bf16 storage.  Activation operands (`act`,
+// `a_plane`) follow ActOut in rg_device.h: fp32 for fp32 models, hi/lo bf16
+// planes a_plane elements apart for bf16 models.
+
+// C[s][m][n] = sum_{k in split s} A[m][k] * W[n][k], fp32 output.
+hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, float* C, int ldc,
+                       int64_t split_stride, const int* d_rows, int rows_ub, int N, int K, int splits,
+                       int k_per_split, hipStream_t st);
+
+// x[r] = embed[tok[r]] (fp32), r < *d_rows.  Prefill: tok = prompts.  An id
+// outside [0, V) reads row 0 instead and sets *bad_token = 1.
+hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_t* tok, float* x,
+                        int32_t* bad_token, const int* d_rows, int rows_ub, hipStream_t st);
+
+// Decode row setup for step t >= 1: row r (< *d_rows) feeds act_tok[r] for
+// sequence s = act_seq[r] at position plen[grp[s]] + t - 1; writes row_tab,
+// row_pos and the embedded token into x.
+hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq,
+                              const int32_t* act_tok, const int32_t* seq_grp, const int32_t* plen, int t,
+                              int32_t* row_tab, int32_t* row_pos, float* x, const int* d_rows,
+                              int rows_ub, hipStream_t st);
+
+// Prefill row setup: row r belongs to prompt p with prompt_off[p] <= r <
+// prompt_off[p+1]; row_tab[r] = tab_base + p, row_pos[r] = r - prompt_off[p].
+hipError_t launch_prefill_rows(const int32_t* prompt_off, int P, int tab_base, int32_t* row_tab,
+                               int32_t* row_pos, int total, hipStream_t st);
+
+// out[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g as an activation operand.  If
+// src_rows != NULL the input row is x[src_rows[r]].
+hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, float eps, void* out, int64_t a_plane,
+                          const int32_t* src_rows, const int* d_rows, int rows_ub, hipStream_t st);
+
+// Sum the GEMM splits of the fused QKV product, rotate q and k, write q (fp32)
+// and append k, v to the row's KV page.
+hipError_t launch_qkv_rope(int dtype, const float* C, int64_t split_stride, int splits, int n_q,
+                           int n_kv, int head_dim, const float* rope_cos, const float* rope_sin,
+                           float* q_out, void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
+                           int tab_stride, const int32_t* row_tab, const int32_t* row_pos,
+                           const int* d_rows, int rows_ub, hipStream_t st);
+
+// Paged causal attention.  Row r's context is positions 0..row_pos[r] of page
+// table row_tab[r]; it is split into n_chunks chunks of chunk_len tokens
+// (a multiple of 256); each (row, kv head, chunk) block writes a partial
+// (max, sum, unnormalised output) per query head.
+hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim,
+                            const void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
+                            int tab_stride, const int32_t* row_tab, const int32_t* row_pos, int chunk_len,
+                            int n_chunks, float* part_o, float* part_ml, const int* d_rows,
+                            int rows_ub, hipStream_t st);
+
+// Merge the chunk partials of each (row, q head) into the activation operand
+// out [rows][n_q*head_dim].
+hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_ml, int n_q,
+                             int head_dim, const int32_t* row_pos, int chunk_len, int n_chunks, void* out,
+                             int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
+
+// x[r][n] += sum_s C[s][r][n]
+hipError_t launch_residual(const float* C, int64_t split_stride, int splits, int N, float* x,
+                           const int* d_rows, int rows_ub, hipStream_t st);
+
+// out[r][j] = silu(g) * u with g = sum_s C[s][r][j], u = sum_s C[s][r][F + j],
+// as an activation operand.
+hipError_t launch_swiglu(int dtype, const float* C, int64_t split_stride, int splits, int F, void* out,
+                         int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
+
+struct SampleArgs {
+  const float* logits;      // [rows][V] or [P][V] when logits_by_group
+  int logits_by_group;      // step 0: logits row = seq_grp[s]
+  int V, eos, t, max_new;
+  uint64_t seed;
+  float temperature;
+  const int32_t* act_seq;   // row -> sequence
+  const int32_t* seq_grp;
+  const int32_t* forced_len;   // device [N] or NULL
+  const int32_t* force_tokens; // device [N*max_new] or NULL
+  float* dump_logits; int dump_steps; int n_seq;
+  int32_t* tokens_out; float* logprobs_out;
+  int32_t* next_tok;        // [rows] token fed to the next step
+  int32_t* done;            // [rows]
+  int32_t* bad_token;       // set to 1 when a forced token id is outside [0, V)
+  const int* d_rows;
+};
+hipError_t launch_sample(const SampleArgs& a, int rows_ub, hipStream_t st);
+
+struct CompactArgs {
+  int t, max_new, page_tok, max_pages, n_seq;
+  int32_t* act_seq; int32_t* act_tok; const int32_t* done;
+  const int32_t* seq_grp; const int32_t* plen;
+  int32_t* page_tab; int32_t* seq_npages; const int32_t* seq_nshared;
+  int32_t* free_stack;
+  int32_t* state;     // [0] active rows, [1] free-stack top, [2] out-of-pages flag
+  int32_t* lengths;
+  int32_t* hist_active; int32_t* hist_groups; int64_t* hist_ctx; int hist_cap;
+};
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
+
+struct ForkArgs {
+  int P, n_seq, page_tok, max_pages, share;
+  const int32_t* grp_off;   // [P+1]
+  const int32_t* plen;      // [P]
+  int32_t* page_tab;        // rows 0..n_seq-1 sequences, n_seq+p prompt tables
+  int32_t* seq_grp; int32_t* seq_npages; int32_t* seq_nshared;
+  int32_t* act_seq;
+  int32_t* free_stack; int32_t* state;
+  int32_t* copy_pairs;      // out: [2*k] (src page, dst page); count in state[3]
+};
+hipError_t launch_fork(const ForkArgs& a, hipStream_t st);
+hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs,
+                            int max_pairs, const int32_t* state, hipStream_t st);
+
+// Rollout set-up: prompt tables, free stack, output padding, counters.
+struct SetupArgs {
+  int P, n_seq, max_new, page_tok, max_pages;
+  int64_t pool_pages;
+  const int32_t* plen; int32_t* prompt_off; int32_t* grp_off; const int32_t* G;
+  int32_t* page_tab; int32_t* free_stack; int32_t* state;
+  int32_t* tokens_out; float* logprobs_out;
+  int32_t* last_rows;      // [P] row of each prompt's last token
+  // state: [0] active rows, [1] free-stack top, [2] out-of-pages flag, [3] page
+  // copies pending, [4] prefix pages, [5] prompt tokens, [6] prompts, [7] invalid token id seen
+};
+hipError_t launch_setup(const SetupArgs& a, hipStream_t st);
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st);
+
+hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P, int N, float eps,
+                                  int ddof, float* adv, hipStream_t st);
+hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,
+                                hipStream_t st);
+hipError_t launch_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* out, hipStream_t st);

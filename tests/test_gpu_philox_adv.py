@@ -1,0 +1,83 @@
+"""GPU parity: Philox blocks and sampling bits bit-exact; group advantage
+within 1e-5 relative of the oracle."""
+import numpy as np
+import pytest
+
+from oracle.philox import philox4x64_10, gumbel_uniform_bits
+from oracle.advantage import group_advantage as oracle_adv
+from workload import get_config, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def rg():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2606_02218_amd as rg
+    return rg
+
+
+def test_philox_blocks_bit_exact(rg):
+    import torch
+    rng = np.random.default_rng(0)
+    ctr = rng.integers(0, 2 ** 63, size=(4096, 4), dtype=np.int64).view(np.uint64)
+    ctr[:8] = np.array([[0, 0, 0, 0], [2 ** 64 - 1] * 4, [1, 2, 3, 4], [5, 0, 17, 0],
+                        [18990, 4095, 511, 0], [0, 1, 0, 0], [7, 7, 7, 7], [2 ** 32, 2 ** 32 - 1, 9, 1]], np.uint64)
+    for key in [(0, 0), (12345, 1), (2 ** 64 - 1, 2 ** 63 + 11)]:
+        dev = torch.from_numpy(ctr.view(np.int64).copy()).cuda()
+        out = rg.philox_blocks(key[0], key[1], dev).cpu().numpy().view(np.uint64)
+        np.testing.assert_array_equal(out, philox4x64_10(ctr, key))
+
+
+@pytest.mark.parametrize("seed,t,s,V", [(0, 0, 0, 512), (1234, 17, 63, 32000), (2 ** 63 + 5, 4095, 511, 151936),
+                                        (7, 8191, 255, 152064)])
+def test_gumbel_bits_bit_exact(rg, seed, t, s, V):
+    got = rg.gumbel_bits(seed, t, s, V).cpu().numpy().view(np.uint32)
+    np.testing.assert_array_equal(got, gumbel_uniform_bits(seed, t, s, V))
+
+
+def _adv_case(rg, rewards, G, ddof=1):
+    import torch
+    r = torch.from_numpy(np.asarray(rewards, np.float32)).cuda()
+    g = torch.from_numpy(np.asarray(G, np.int32)).cuda()
+    got = rg.group_advantage(r, g, 1e-6, ddof).cpu().numpy()
+    ref = oracle_adv(np.asarray(rewards, np.float32), G, np.float32(1e-6), ddof)
+    np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-7)
+    return got
+
+
+@pytest.mark.parametrize("ddof", [0, 1])
+def test_advantage_layouts(rg, ddof):
+    rng = np.random.default_rng(1)
+    layouts = [[4] * 8, [16] * 32, list(make_inputs(get_config("1.5b-dyn"), 0).G), [1, 2, 3, 1000, 5],
+               list(rng.integers(1, 9, size=3000)), [1]]
+    for G in layouts:
+        N = int(np.sum(G))
+        _adv_case(rg, (rng.random(N) < 0.5).astype(np.float32), G, ddof)
+        _adv_case(rg, rng.normal(size=N).astype(np.float32), G, ddof)
+
+
+def test_advantage_constant_groups_and_invariants(rg):
+    G = [4, 4, 8, 2]
+    r = np.array([1, 1, 1, 1, 0, 0, 0, 0] + [1, 0, 0, 1, 1, 1, 0, 0] + [3, 3], np.float32)
+    a = _adv_case(rg, r, G)
+    assert np.all(a[:8] == 0) and np.all(a[-2:] == 0)
+    seg = a[8:16].astype(np.float64)
+    assert abs(seg.sum()) < 1e-6 * 8
+    sd = np.std(r[8:16].astype(np.float64), ddof=1)
+    assert abs(np.std(seg, ddof=1) - sd / (sd + 1e-6)) < 1e-6
+
+
+def test_advantage_workload_rewards(rg):
+    for name in ["tiny", "gpt2s", "1.5b", "1.5b-dyn", "7b"]:
+        inp = make_inputs(get_config(name), 0)
+        _adv_case(rg, inp.rewards, list(inp.G))
+
+
+def test_advantage_bad_group_sizes_give_nan(rg):
+    import torch
+    r = torch.ones(8, device="cuda")
+    for G in ([4, 3], [4, 0, 4], [4, 5]):
+        out = rg.group_advantage(r, torch.tensor(G, dtype=torch.int32, device="cuda")).cpu().numpy()
+        assert np.all(np.isnan(out)), G
