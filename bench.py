@@ -1,0 +1,193 @@
+"""Group-step benchmark of the rollout hot path on one MI355X.
+
+One step = rollout_group (prefill, fork, decode until every sequence retires)
++ group_advantage over one batch of the 1.5B-shaped workload: 32 prompts x
+G = 16 siblings, 512-token prompts, max_new 4096, forced lognormal(ln 1200, 0.8)
+lengths, bf16 random-init weights.  Inputs are resident in HBM before timing.
+Prints one JSON line (see the keys below).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12            # MI355X HBM3E, bytes/s
+MFMA_BF16_PEAK = 2.5e15      # dense bf16 MFMA, flop/s
+
+
+def algorithmic_bytes(shape, hist_active, hist_groups, hist_ctx, plen):
+    """Per decode step t >= 1 (rows A_t, groups g_t), the bytes the method must
+    move, split by kernel class.  Weights once per step; KV: each active
+    group's prompt prefix once plus each row's own t generated tokens;
+    activations in/out of every projection (fp32)."""
+    L, d, F, V = shape.n_layers, shape.d_model, shape.ffn_dim, shape.vocab
+    wb = shape.elem_bytes
+    kvb = shape.elem_bytes
+    qd, kvd = shape.q_dim, shape.kv_dim
+    kv_tok_layer = 2 * kvd * kvb
+    out = {"gemm_qkv": 0.0, "gemm_o": 0.0, "gemm_gu": 0.0, "gemm_down": 0.0, "gemm_lm": 0.0, "attn": 0.0}
+    launches = {k: 0 for k in out}
+    for t in range(1, len(hist_active)):
+        M = int(hist_active[t])
+        if M == 0:
+            break
+        g = int(hist_groups[t])
+        prefix = float(hist_ctx[t]) / M * g if M else 0.0      # sum over active groups of Lp (uniform Lp here)
+        ctx_tokens = prefix + M * t                              # prefix once per group + own tokens
+        out["gemm_qkv"] += L * ((qd + 2 * kvd) * d * wb + M * d * 4 + M * (qd + 2 * kvd) * 4)
+        out["gemm_o"] += L * (d * qd * wb + M * qd * 4 + M * d * 4)
+        out["gemm_gu"] += L * (2 * F * d * wb + M * d * 4 + M * 2 * F * 4)
+        out["gemm_down"] += L * (d * F * wb + M * F * 4 + M * d * 4)
+        out["gemm_lm"] += V * d * wb + M * d * 4 + M * V * 4
+        out["attn"] += L * (ctx_tokens * kv_tok_layer + M * qd * 4 * 2)
+        for k in ("gemm_qkv", "gemm_o", "gemm_gu", "gemm_down", "attn"):
+            launches[k] += L
+        launches["gemm_lm"] += 1
+    return out, launches
+
+
+def decode_bytes_total(shape, hist_active, hist_groups, hist_ctx):
+    """SURVEY-style whole-step decode bytes: weights + KV read + per-row write."""
+    W = shape.decode_weight_bytes()
+    kv_tok = shape.kv_bytes_per_token()
+    tot = 0.0
+    for t in range(1, len(hist_active)):
+        M = int(hist_active[t])
+        if M == 0:
+            break
+        g = int(hist_groups[t])
+        prefix = float(hist_ctx[t]) / M * g
+        tot += W + kv_tok * (prefix + M * t) + M * (kv_tok + shape.d_model * shape.elem_bytes + 8)
+    return tot
+
+
+def cpu_baseline(wl, weights, inputs, n_steps: int):
+    """The oracle on the host: prefill of prompt 0 plus its G siblings for
+    n_steps decode steps (a bounded sample of the same workload)."""
+    from oracle.model import OracleModel
+    from oracle.rollout import rollout as oracle_rollout
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        threads = max([i.get("num_threads", 0) for i in info] or [0]) or None
+    except Exception:
+        pass
+    if threads is None:
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    model = OracleModel(wl.shape, weights)
+    t0 = time.perf_counter()
+    out = oracle_rollout(model, inputs.prompts, inputs.G, wl.max_new, 1234, inputs.forced_len,
+                         max_steps=n_steps, prompt_subset=[0])
+    dt = time.perf_counter() - t0
+    gen = int(np.sum(out["tokens"][: int(inputs.G[0])] >= 0))
+    return {"value": gen / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"prompt 0 of the same workload: prefill {wl.prompt_len} tokens + {int(inputs.G[0])} siblings "
+                      f"x {n_steps} decode steps ({gen} tokens) in {dt:.1f} s, float64 numpy"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="1.5b")
+    ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
+    ap.add_argument("--cpu-steps", type=int, default=6, help="decode steps of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (groups would shard across GPUs "
+              "by prompt; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_02218_amd as rg
+    from workload import get_config, make_weights, make_inputs
+
+    wl = get_config(args.workload)
+    shape = wl.shape
+    weights = make_weights(shape, 0)
+    inp = make_inputs(wl, 0)
+    N = inp.n_seq
+    pol = rg.Policy(shape, weights, max_seqs=N, max_prompts=wl.n_prompts,
+                    max_prompt_tokens=wl.n_prompts * wl.prompt_len, max_context=wl.prompt_len + wl.max_new)
+    dev = torch.device("cuda")
+    prompts = torch.from_numpy(inp.prompts).to(dev)
+    G_dev = torch.from_numpy(inp.G).to(dev)
+    rewards = torch.from_numpy(inp.rewards).to(dev)
+    tokens = torch.empty((N, wl.max_new), dtype=torch.int32, device=dev)
+    lengths = torch.empty(N, dtype=torch.int32, device=dev)
+    logprobs = torch.empty((N, wl.max_new), dtype=torch.float32, device=dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    profile = not args.no_profile
+
+    def step(i, prof):
+        pol.rollout(prompts, inp.G, wl.max_new, 1234 + i, forced_len=inp.forced_len, profile=prof,
+                    out=(tokens, lengths, logprobs))
+        rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)
+
+    for i in range(args.warmup):
+        step(i, False)
+        print(f"# warmup step {i} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    kt = {}
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, profile)
+        if profile:
+            for k, (ms, n) in pol.kernel_times(1).items():
+                a = kt.setdefault(k, [0.0, 0])
+                a[0] += ms
+                a[1] += n
+        print(f"# timed step {i} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    gen = int(lengths.sum().item()) * 1  # tokens of the last step; every step has the same forced lengths
+    hist_a, hist_g, hist_c = pol.step_history()
+    assert np.array_equal(lengths.cpu().numpy(), inp.forced_len), "retired lengths differ from the forced lengths"
+
+    ms_per_step = dt / args.steps * 1e3
+    value = gen / (ms_per_step / 1e3)
+    res = {"metric": "rollout decode tokens/s (group step = rollout_group + group_advantage)",
+           "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_per_step, 2), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": wl.name, "prompts": wl.n_prompts, "group_size": int(inp.G[0]),
+                      "sequences": N, "prompt_len": wl.prompt_len, "max_new": wl.max_new,
+                      "generated_tokens": gen, "decode_steps": int(len(hist_a))},
+           "group_step_s": round(ms_per_step / 1e3, 4)}
+    if profile and kt:
+        alg, _ = algorithmic_bytes(shape, hist_a, hist_g, hist_c, wl.prompt_len)
+        dec_ms = sum(v[0] for v in kt.values()) / args.steps
+        # dominant kernel class over the decode steps
+        dom = max(kt.items(), key=lambda kv: kv[1][0])
+        name, (ms_tot, n_tot) = dom
+        ms_avg = ms_tot / max(1, n_tot)
+        res["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 2) for k, v in sorted(kt.items(), key=lambda kv: -kv[1][0])}
+        if name in alg:
+            per_launch = alg[name] * args.steps / max(1, n_tot)
+            achieved = per_launch / (ms_avg / 1e3)
+            res["roofline"] = {"kernel": name, "bound": "hbm", "achieved": round(achieved / 1e9, 1),
+                               "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4),
+                               "traffic": None, "avg_launch_us": round(ms_avg * 1e3, 2),
+                               "alg_bytes_per_launch": round(per_launch)}
+        tot_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
+        res["decode_hbm_frac_kernel_time"] = round(tot_b / (dec_ms / 1e3) / HBM_PEAK, 4)
+    if not args.no_cpu_baseline:
+        del pol
+        torch.cuda.empty_cache()
+        res["cpu_baseline"] = cpu_baseline(wl, weights, inp, args.cpu_steps)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
