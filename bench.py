@@ -98,12 +98,24 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=1, help="untimed steps; the first one times every kernel class")
     ap.add_argument("--workload", default="1.5b")
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
-    ap.add_argument("--cpu-steps", type=int, default=6, help="decode steps of the oracle baseline sample")
+    ap.add_argument("--cpu-steps", type=int, default=32, help="decode steps of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calib:
+        import torch
+        n = args.copy_calib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calib_bytes_per_copy": n * 4, "copies": 5}))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (groups would shard across GPUs "
               "by prompt; see the design notes).", file=sys.stderr)
@@ -135,19 +147,27 @@ def main():
                     out=(tokens, lengths, logprobs))
         rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)
 
+    breakdown, dom = {}, None
     for i in range(args.warmup):
-        step(i, False)
+        # the first warmup step times every kernel class (untimed step): the
+        # per-class breakdown, and the dominant class timed in the timed steps
+        step(i, profile and i == 0)
+        if profile and i == 0:
+            breakdown = pol.kernel_times(1)
+            dom = max(breakdown.items(), key=lambda kv: kv[1][0])[0]
         print(f"# warmup step {i} done", file=sys.stderr, flush=True)
+    if profile and dom is None:
+        dom = "attn"
     torch.cuda.synchronize()
     kt = {}
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, profile)
+        step(args.warmup + i, [dom] if profile else False)
         if profile:
-            for k, (ms, n) in pol.kernel_times(1).items():
-                a = kt.setdefault(k, [0.0, 0])
-                a[0] += ms
-                a[1] += n
+            ms, n = pol.kernel_times(1)[dom]
+            a = kt.setdefault(dom, [0.0, 0])
+            a[0] += ms
+            a[1] += n
         print(f"# timed step {i} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
@@ -165,23 +185,23 @@ def main():
                       "sequences": N, "prompt_len": wl.prompt_len, "max_new": wl.max_new,
                       "generated_tokens": gen, "decode_steps": int(len(hist_a))},
            "group_step_s": round(ms_per_step / 1e3, 4)}
+    if breakdown:
+        res["kernel_ms_breakdown_untimed_step"] = {k: round(v[0], 1) for k, v in
+                                                   sorted(breakdown.items(), key=lambda kv: -kv[1][0]) if v[1]}
+        dec_ms = sum(v[0] for v in breakdown.values())
+        tot_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
+        res["decode_hbm_frac_kernel_time"] = round(tot_b / (dec_ms / 1e3) / HBM_PEAK, 4)
     if profile and kt:
         alg, _ = algorithmic_bytes(shape, hist_a, hist_g, hist_c, wl.prompt_len)
-        dec_ms = sum(v[0] for v in kt.values()) / args.steps
-        # dominant kernel class over the decode steps
-        dom = max(kt.items(), key=lambda kv: kv[1][0])
-        name, (ms_tot, n_tot) = dom
+        name, (ms_tot, n_tot) = next(iter(kt.items()))
         ms_avg = ms_tot / max(1, n_tot)
-        res["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 2) for k, v in sorted(kt.items(), key=lambda kv: -kv[1][0])}
         if name in alg:
             per_launch = alg[name] * args.steps / max(1, n_tot)
             achieved = per_launch / (ms_avg / 1e3)
             res["roofline"] = {"kernel": name, "bound": "hbm", "achieved": round(achieved / 1e9, 1),
                                "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4),
                                "traffic": None, "avg_launch_us": round(ms_avg * 1e3, 2),
-                               "alg_bytes_per_launch": round(per_launch)}
-        tot_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
-        res["decode_hbm_frac_kernel_time"] = round(tot_b / (dec_ms / 1e3) / HBM_PEAK, 4)
+                               "alg_bytes_per_launch": round(per_launch), "launches": n_tot}
     if not args.no_cpu_baseline:
         del pol
         torch.cuda.empty_cache()

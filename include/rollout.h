@@ -53,18 +53,21 @@ extern "C" {
  * tokens are at positions 0..Lp-1, generated token t at Lp+t.  Query head h
  * reads key/value head floor(h*n_kv_heads/n_q_heads).  MLP =
  * W_down(silu(W_gate x) * (W_up x)).
- * Supported: head_dim even and <= 256, n_q_heads a multiple of n_kv_heads,
- * d_model, n_q_heads*head_dim and ffn_dim multiples of 32, vocab a multiple
- * of 16 (otherwise RG_EUNSUPPORTED). */
+ * Supported: head_dim a multiple of 8 and <= 256 (bf16 models: 64, 128 or
+ * 256), n_q_heads a multiple of n_kv_heads with at most 8 query heads per kv
+ * head, d_model, n_q_heads*head_dim and ffn_dim multiples of 64, vocab a
+ * multiple of 16 (otherwise RG_EUNSUPPORTED). */
 typedef struct rg_config {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
   int32_t eos_id;       /* token that ends a completion, in [0, vocab)                   */
   float rope_theta;
   float rms_eps;
-  int32_t dtype;        /* RG_DTYPE_F32: fp32 matrices and KV.  RG_DTYPE_BF16: bf16
-                           matrices and KV, bf16 GEMM operands (activations rounded to
-                           nearest-even bf16 at each matrix-product input, keys after
-                           RoPE), fp32 residual, norms, attention and accumulation.      */
+  int32_t dtype;        /* RG_DTYPE_F32: fp32 matrices and KV cache.  RG_DTYPE_BF16: bf16
+                           matrices and KV cache (keys rounded to nearest-even bf16 after
+                           RoPE, values after projection); every other value is fp32.
+                           bf16 MFMA takes each fp32 activation as a hi + lo pair of bf16
+                           values (about 17 significant bits), so products keep the
+                           activation's fp32 precision.                                  */
 } rg_config;
 
 /* Weights, all DEVICE pointers, read during rg_policy_create only (the policy
@@ -103,8 +106,9 @@ typedef struct rg_policy rg_policy;  /* opaque: packed weights, KV pool, workspa
 /* Flags for rg_sampling.flags */
 #define RG_FLAG_NO_PREFIX_SHARING 1  /* give every sibling private copies of its prompt's
                                         KV pages (results are bit-identical; a test aid) */
-#define RG_FLAG_PROFILE           2  /* time every kernel launch with HIP events; read the
-                                        totals with rg_kernel_times()                    */
+#define RG_FLAG_PROFILE           2  /* time kernel launches with HIP events (the classes in
+                                        rg_sampling.profile_kinds, all when it is 0); read
+                                        the totals with rg_kernel_times()                */
 
 /* Sampling options.  A NULL rg_sampling* means temperature 1, natural EOS, no
  * flags.  Token t of sequence s is argmax_v fp32(z_v/T) + g_v where g_v is the
@@ -126,6 +130,8 @@ typedef struct rg_sampling {
                                    sequence s at step t < dump_steps go to
                                    dump_logits[(t*N+s)*vocab ...]; untouched otherwise     */
   int32_t dump_steps;
+  uint32_t profile_kinds;       /* with RG_FLAG_PROFILE: bit k times kernel class k
+                                   (RG_K_*); 0 times every class                           */
 } rg_sampling;
 
 const char* rg_last_error(void);

@@ -49,7 +49,8 @@ class rg_limits(C.Structure):
 
 class rg_sampling(C.Structure):
     _fields_ = [("temperature", C.c_float), ("flags", C.c_int32), ("forced_len", C.POINTER(C.c_int32)),
-                ("force_tokens", C.c_void_p), ("dump_logits", C.c_void_p), ("dump_steps", C.c_int32)]
+                ("force_tokens", C.c_void_p), ("dump_logits", C.c_void_p), ("dump_steps", C.c_int32),
+                ("profile_kinds", C.c_uint32)]
 
 
 def lib_path() -> str:
@@ -158,10 +159,12 @@ class Policy:
 
     def rollout(self, prompts, G: Sequence[int], max_new: int, seed: int, temperature: float = 1.0,
                 forced_len=None, force_tokens=None, dump_steps: int = 0, share_prefix: bool = True,
-                profile: bool = False, out=None, stream=None):
+                profile=False, out=None, stream=None):
         """prompts: device int32 tensor [P, Lp] or a list of 1-D device int32
         tensors.  Returns (tokens [N, max_new], lengths [N], logprobs
-        [N, max_new]) and, with dump_steps, the logits [dump_steps, N, V]."""
+        [N, max_new]) and, with dump_steps, the logits [dump_steps, N, V].
+        ``profile``: False, True (time every kernel class) or an iterable of
+        class names from KERNEL_KINDS to time."""
         import torch
         lib = load_library()
         if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
@@ -184,6 +187,10 @@ class Policy:
             tokens, lengths, logprobs = out
         dump = torch.empty((dump_steps, N, self.shape.vocab), dtype=torch.float32, device=dev) if dump_steps else None
         flags = (0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+        kinds = 0
+        if profile and profile is not True:
+            for name in profile:
+                kinds |= 1 << KERNEL_KINDS.index(name)
         fl = None
         if forced_len is not None:
             fl_np = np.ascontiguousarray(np.asarray(forced_len, dtype=np.int32))
@@ -191,7 +198,7 @@ class Policy:
         ft = None
         if force_tokens is not None:
             ft = force_tokens.to(device=dev, dtype=torch.int32).contiguous()
-        opts = rg_sampling(float(temperature), flags, fl, _ptr(ft), _ptr(dump), dump_steps)
+        opts = rg_sampling(float(temperature), flags, fl, _ptr(ft), _ptr(dump), dump_steps, kinds)
         plen_a = (C.c_int32 * P)(*plen)
         g_a = (C.c_int32 * P)(*G)
         _check(lib.rollout_group(self._h, _ptr(packed), plen_a, P, g_a, max_new, C.c_uint64(seed & (2 ** 64 - 1)),

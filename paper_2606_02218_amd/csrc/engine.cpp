@@ -39,9 +39,9 @@ int fail(int code, const std::string& msg) {
   } while (0)
 
 constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
-constexpr int RG_SPLIT_MAX = 16;       // largest split-K factor of a decode GEMM
+constexpr int RG_SPLIT_MAX = 32;       // largest split-K factor of a decode GEMM
 constexpr int RG_GEMM_TARGET = 1024;   // blocks a GEMM launch aims for
-constexpr int RG_ATT_TARGET = 1024;    // blocks an attention launch aims for
+constexpr int RG_ATT_TARGET = 4096;    // work items an attention launch aims for
 constexpr int RG_RING = 64;            // async active-count slots
 constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
 constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
@@ -97,6 +97,7 @@ struct rg_policy {
 
   // profiling
   bool prof = false;
+  uint32_t prof_mask = 0xFFFFFFFFu;
   int prof_phase = 0;
   std::vector<hipEvent_t> prof_ev;  // 2 * RG_PROF_RING
   std::vector<int> prof_kind, prof_ph;
@@ -144,7 +145,7 @@ struct ProfScope {
   int64_t slot = -1;
   int rc = RG_OK;
   ProfScope(rg_policy* pol, hipStream_t s, int kind) : p(pol), st(s) {
-    if (!p->prof) return;
+    if (!p->prof || !((p->prof_mask >> kind) & 1u)) return;
     if (p->prof_head - p->prof_tail >= RG_PROF_RING) rc = prof_drain_one(p);
     slot = p->prof_head % RG_PROF_RING;
     p->prof_kind[slot] = kind;
@@ -166,14 +167,20 @@ struct ProfScope {
     if (e_ != hipSuccess) return fail(RG_EHIP, std::string("launch ") + #kind + ": " + hipGetErrorString(e_)); \
   } while (0)
 
+// Split-K factor of a projection: enough blocks to cover the chip, each split
+// at least two 64-wide K steps, and split partials (written and read back as
+// fp32) no more than the weight bytes (S * rows * 4 <= K).
 void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits, int* kps) {
   int S = 1;
   if (pol->dtype == RG_DTYPE_BF16) {
-    const int64_t blocks = ceil_div(N, 64) * ceil_div(rows_ub, 64);
-    if (blocks < RG_GEMM_TARGET) S = (int)std::min<int64_t>(ceil_div(RG_GEMM_TARGET, blocks), K / 256);
-    S = std::max(1, std::min(S, RG_SPLIT_MAX));
+    const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub), bn = gemm_tile_cols(pol->dtype, rows_ub);
+    const int64_t blocks = ceil_div(N, bn) * ceil_div(rows_ub, bm);
+    if (blocks < RG_GEMM_TARGET) S = (int)ceil_div(RG_GEMM_TARGET, blocks);
+    S = (int)std::min<int64_t>({(int64_t)S, K / 128, std::max<int64_t>(1, K / (4LL * rows_ub)), RG_SPLIT_MAX});
+    S = std::max(1, S);
   }
-  int k = (int)ceil_div(ceil_div(K, S), 32) * 32;
+  const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
+  int k = (int)(ceil_div(ceil_div(K, S), step) * step);
   *kps = k;
   *splits = (int)ceil_div(K, k);
 }
@@ -185,8 +192,9 @@ int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const v
     choose_splits(pol, N, rows_ub, K, &S, &kps);
     const int64_t fit = pol->cpart_elems / ((int64_t)rows_ub * N);   // splits the workspace holds
     if (S > fit) {
+      const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
       S = (int)std::max<int64_t>(1, fit);
-      kps = (int)ceil_div(ceil_div(K, S), 32) * 32;
+      kps = (int)ceil_div(ceil_div(K, S), step) * step;
       S = (int)ceil_div(K, kps);
     }
   } else {   // direct output (the lm head into the logits buffer): never split
@@ -279,10 +287,12 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       c.vocab < 2 || c.eos_id < 0 || c.eos_id >= c.vocab || !(c.rope_theta > 0.f) || !(c.rms_eps >= 0.f))
     return fail(RG_EINVAL, "rg_policy_create: invalid config");
   if (c.dtype != RG_DTYPE_F32 && c.dtype != RG_DTYPE_BF16) return fail(RG_EUNSUPPORTED, "unsupported dtype");
+  if (c.dtype == RG_DTYPE_BF16 && c.head_dim != 64 && c.head_dim != 128 && c.head_dim != 256)
+    return fail(RG_EUNSUPPORTED, "unsupported shape: bf16 models need head_dim 64, 128 or 256");
   if (c.head_dim % 8 || c.head_dim > 256 || c.n_q_heads % c.n_kv_heads || c.n_q_heads / c.n_kv_heads > 8 ||
-      c.d_model % 32 || (c.n_q_heads * c.head_dim) % 32 || c.ffn_dim % 32 || c.vocab % 16)
+      c.d_model % 64 || (c.n_q_heads * c.head_dim) % 64 || c.ffn_dim % 64 || c.vocab % 16)
     return fail(RG_EUNSUPPORTED, "unsupported shape: need head_dim%8==0, head_dim<=256, n_q/n_kv integer <= 8, "
-                                 "d_model, n_q*head_dim, ffn_dim multiples of 32, vocab multiple of 16");
+                                 "d_model, n_q*head_dim, ffn_dim multiples of 64, vocab multiple of 16");
   const rg_limits lim = *limits;
   if (lim.max_seqs < 1 || lim.max_prompts < 1 || lim.max_prompt_tokens < 1 || lim.max_context < 2 ||
       lim.kv_pool_pages < 0)
@@ -473,6 +483,7 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
 
   // profiling state
   pol->prof = (o.flags & RG_FLAG_PROFILE) != 0;
+  pol->prof_mask = o.profile_kinds ? o.profile_kinds : 0xFFFFFFFFu;
   if (pol->prof) {
     if (pol->prof_ev.empty()) {
       pol->prof_ev.resize(2 * RG_PROF_RING);

@@ -1,11 +1,19 @@
 // Paged causal attention over the KV pool, for prefill rows and decode rows
-// alike.  Each block handles (row, kv head, chunk of the row's context): it
-// scores up to 256 context tokens per tile against the GQA group's query heads
-// (fp32, keys/values converted from the storage type), keeps a running
-// softmax (max, sum) and accumulates the unnormalised output; the merge kernel
-// combines the chunks.  Context positions 0..row_pos[r] of page table
-// row_tab[r]; position j lives in page page_tab[tab*tab_stride + j/page_tok],
-// slot j % page_tok.
+// alike.  Work item = (row, kv head, chunk of the row's context); it keeps a
+// running softmax (max, sum) and an unnormalised output per query head of the
+// GQA group, and the merge kernel combines the chunks.  Context positions
+// 0..row_pos[r] of page table row_tab[r]; position j lives in page
+// page_tab[tab*tab_stride + j/page_tok], slot j % page_tok.  Inside a page a
+// layer holds K as [kv head][slot][dim] and V transposed, [kv head][dim][slot].
+//
+// bf16 KV: one wave per work item on MFMA 16x16x32.  Scores are formed
+// transposed, S^T = K Q^T (tokens x query heads), so each lane ends up holding
+// the probabilities of one query head for 8 tokens -- exactly a B fragment of
+// O^T = V^T P^T (the 8 tokens of a 32-token block are taken in the order the
+// S^T layout leaves them: 4g..4g+3 and 16+4g..16+4g+3 for lane group g, and
+// the V^T fragment is loaded in the same order).  q and p are fp32 values
+// split into hi/lo bf16 pairs, so both products keep fp32-level accuracy.
+// fp32 KV (fp32 models): a plain per-token VALU kernel.
 #include "rg_device.h"
 #include "rg_kernels.h"
 
@@ -60,7 +68,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
   if (tid < rep) { s_m[tid] = -INFINITY; s_l[tid] = 0.f; }
   const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
   const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * g.page_tok * hd;
-  const int64_t voff = koff + (int64_t)n_kv * g.page_tok * hd;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * g.page_tok * hd;   // V^T [dim][slot]
 
   // each thread owns output slots (h, d) = idx / hd, idx % hd for idx = tid + 256*k
   const int n_slots = (rep * hd + 255) / 256;
@@ -118,8 +126,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
         float a = acc[k] * s_alpha[h];
         for (int jj = 0; jj < nt; ++jj) {
           const int j = t0 + jj;
-          const KV* vp = pool + (int64_t)tab[j / g.page_tok] * g.page_elems + voff + (int64_t)(j % g.page_tok) * hd;
-          a = fmaf(sp[h * ATT_TILE + jj], ld_f32<KV>(vp + d), a);
+          const KV* vp = pool + (int64_t)tab[j / g.page_tok] * g.page_elems + voff + (int64_t)d * g.page_tok;
+          a = fmaf(sp[h * ATT_TILE + jj], ld_f32<KV>(vp + (j % g.page_tok)), a);
         }
         acc[k] = a;
       }
@@ -135,6 +143,165 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
   if (tid < rep) {
     part_ml[(base + tid) * 2] = s_m[tid];
     part_ml[(base + tid) * 2 + 1] = s_l[tid];
+  }
+}
+
+
+// ---------------------------------------------------------------- MFMA path
+__device__ __forceinline__ void split8(const float* v, bf16x8_t& hi, bf16x8_t& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16_t h0 = f32_to_bf16(v[2 * i]), h1 = f32_to_bf16(v[2 * i + 1]);
+    const bf16_t l0 = f32_to_bf16(v[2 * i] - bf16_to_f32(h0)), l1 = f32_to_bf16(v[2 * i + 1] - bf16_to_f32(h1));
+    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  hi = __builtin_bit_cast(bf16x8_t, uint4{h[0], h[1], h[2], h[3]});
+  lo = __builtin_bit_cast(bf16x8_t, uint4{l[0], l[1], l[2], l[3]});
+}
+
+template <int HD>
+__global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
+                                                       const bf16_t* __restrict__ pool, KvGeom g, int layer,
+                                                       const int32_t* __restrict__ page_tab, int tab_stride,
+                                                       const int32_t* __restrict__ row_tab,
+                                                       const int32_t* __restrict__ row_pos, int chunk_len,
+                                                       int n_chunks, int rows_ub, float* __restrict__ part_o,
+                                                       float* __restrict__ part_ml, const int* __restrict__ d_rows) {
+  static_assert(HD % 32 == 0 && HD <= 256, "head_dim");
+  // XCD-aware order: the 1-D grid has a multiple of 8 blocks and blocks are
+  // dealt to the 8 XCDs round-robin, so XCD x = b % 8 takes the contiguous
+  // work range [x*per_xcd, (x+1)*per_xcd): neighbouring rows (siblings of one
+  // prompt) share an XCD, whose L2 then holds their shared prefix.
+  const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
+  const int64_t b = blockIdx.x;
+  const int64_t per_xcd = (int64_t)gridDim.x / 8;
+  const int64_t w = (b % 8) * per_xcd + b / 8;
+  if (w >= nb) return;
+  const int chunk = (int)(w % n_chunks);
+  const int kvh = (int)((w / n_chunks) % n_kv);
+  const int r = (int)(w / ((int64_t)n_chunks * n_kv));
+  if (r >= *d_rows) return;
+  const int ctx = row_pos[r] + 1;
+  const int c0 = chunk * chunk_len;
+  if (c0 >= ctx) return;
+  const int c1 = min(ctx, c0 + chunk_len);
+  const int rep = n_q / n_kv;
+  const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
+  const int PT = g.page_tok;   // 16
+
+  // Q^T fragments: lane holds q[head col][kb*32 + 8*grp + 0..7], pre-scaled by 1/sqrt(hd)
+  bf16x8_t qh[HD / 32], ql[HD / 32];
+  {
+    const float scale = 1.0f / sqrtf((float)HD);
+    const float* qr = q + ((int64_t)r * n_q + kvh * rep + min(col, rep - 1)) * HD + 8 * grp;   // lanes >= rep: padding
+#pragma unroll
+    for (int kb = 0; kb < HD / 32; ++kb) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = col < rep ? qr[kb * 32 + i] * scale : 0.f;
+      split8(v, qh[kb], ql[kb]);
+    }
+  }
+  const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
+  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * PT * HD;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * PT * HD;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t oacc[HD / 16];
+#pragma unroll
+  for (int i = 0; i < HD / 16; ++i) oacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int t0 = c0; t0 < c1; t0 += 32) {
+    // ---- S^T for tokens t0..t0+31 (two 16-token tiles)
+    f32x4_t s[2];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      int tok = t0 + tt * 16 + col;
+      if (tok >= c1) tok = c0;                     // keep the load in bounds; masked below
+      const bf16_t* kp = pool + (int64_t)tab[tok / PT] * g.page_elems + koff + (int64_t)(tok % PT) * HD + 8 * grp;
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < HD / 32; ++kb) {
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kp + kb * 32));
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[kb], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[kb], acc, 0, 0, 0);
+      }
+      s[tt] = acc;
+    }
+    // ---- online softmax for query head `col`: lane holds tokens t0 + tt*16 + 4*grp + j
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int tok = t0 + tt * 16 + 4 * grp + j;
+        if (tok >= c1) s[tt][j] = -INFINITY;
+        mloc = fmaxf(mloc, s[tt][j]);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m_run, mloc);
+    const float alpha = expf(m_run - m_new);       // 0 on the first block
+    float p[8];
+    float psum = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float e = expf(s[tt][j] - m_new);    // exp(-inf) = 0 for masked tokens
+        p[tt * 4 + j] = e;
+        psum += e;
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) oacc[i] *= alpha;
+    bf16x8_t ph, pl;
+    split8(p, ph, pl);
+    // ---- O^T += V^T P^T; V^T fragment rows = dims, k = the same 8 tokens
+    const int pg0 = tab[t0 / PT];
+    const int pg1 = (t0 + 16 < c1) ? tab[t0 / PT + 1] : pg0;
+    const int nval0 = min(4, max(0, c1 - (t0 + 4 * grp)));          // valid tokens among 4*grp..+3
+    const int nval1 = min(4, max(0, c1 - (t0 + 16 + 4 * grp)));
+    const bf16_t* v0 = pool + (int64_t)pg0 * g.page_elems + voff + 4 * grp;
+    const bf16_t* v1 = pool + (int64_t)pg1 * g.page_elems + voff + 4 * grp;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const int dim = dt * 16 + col;
+      uint2 a0 = *reinterpret_cast<const uint2*>(v0 + (int64_t)dim * PT);
+      uint2 a1 = *reinterpret_cast<const uint2*>(v1 + (int64_t)dim * PT);
+      // zero the slots of masked tokens (their memory may hold anything)
+      if (nval0 < 4) {
+        const uint64_t keep = nval0 == 0 ? 0ull : (~0ull >> (64 - 16 * nval0));
+        const uint64_t v = ((uint64_t)a0.y << 32 | a0.x) & keep;
+        a0 = uint2{(uint32_t)v, (uint32_t)(v >> 32)};
+      }
+      if (nval1 < 4) {
+        const uint64_t keep = nval1 == 0 ? 0ull : (~0ull >> (64 - 16 * nval1));
+        const uint64_t v = ((uint64_t)a1.y << 32 | a1.x) & keep;
+        a1 = uint2{(uint32_t)v, (uint32_t)(v >> 32)};
+      }
+      const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, uint4{a0.x, a0.y, a1.x, a1.y});
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, oacc[dt], 0, 0, 0);
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, oacc[dt], 0, 0, 0);
+    }
+  }
+  // ---- partials: lane holds O^T[dims dt*16 + 4*grp + j][head col]
+  if (col < rep) {
+    const int64_t base = ((int64_t)r * n_chunks + chunk) * n_q + kvh * rep + col;
+    float* po = part_o + base * HD;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) po[dt * 16 + 4 * grp + j] = oacc[dt][j];
+    if (grp == 0) {
+      part_ml[base * 2] = m_run;
+      part_ml[base * 2 + 1] = l_run;
+    }
   }
 }
 
@@ -172,11 +339,22 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
                             float* part_o, float* part_ml, const int* d_rows, int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
   dim3 grid(n_chunks, n_kv, rows_ub);
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_attention<bf16_t>, grid, dim3(256), 0, st, q, n_q, n_kv, head_dim, (const bf16_t*)kv_pool,
-                       g, layer, page_tab, tab_stride, row_tab, row_pos, chunk_len, n_chunks, part_o, part_ml,
-                       d_rows);
-  else
+  if (dtype == 1) {
+    // two 16-slot pages per 32-token block, blocks 32-aligned inside a chunk
+    if (g.page_tok != 16 || chunk_len % 32 != 0) return hipErrorInvalidValue;
+    const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
+    const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
+#define RG_ATT_MFMA(HD)                                                                                          \
+    hipLaunchKernelGGL(k_attention_mfma<HD>, grid1, dim3(64), 0, st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
+                       page_tab, tab_stride, row_tab, row_pos, chunk_len, n_chunks, rows_ub, part_o, part_ml, d_rows)
+    switch (head_dim) {
+      case 64: RG_ATT_MFMA(64); break;
+      case 128: RG_ATT_MFMA(128); break;
+      case 256: RG_ATT_MFMA(256); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef RG_ATT_MFMA
+  } else
     hipLaunchKernelGGL(k_attention<float>, grid, dim3(256), 0, st, q, n_q, n_kv, head_dim, (const float*)kv_pool,
                        g, layer, page_tab, tab_stride, row_tab, row_pos, chunk_len, n_chunks, part_o, part_ml,
                        d_rows);

@@ -81,8 +81,8 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const float* __restrict__ C, i
   const int pos = row_pos[r];
   const int page = page_tab[(int64_t)row_tab[r] * tab_stride + pos / g.page_tok];
   const int slot = pos % g.page_tok;
-  KV* kbase = pool + (int64_t)page * g.page_elems + (int64_t)layer * g.layer_elems;
-  KV* vbase = kbase + (int64_t)n_kv * g.page_tok * hd;
+  KV* kbase = pool + (int64_t)page * g.page_elems + (int64_t)layer * g.layer_elems;   // K [head][slot][dim]
+  KV* vbase = kbase + (int64_t)n_kv * g.page_tok * hd;                                 // V^T [head][dim][slot]
   const float* cs = rope_cos + (int64_t)pos * half;
   const float* sn = rope_sin + (int64_t)pos * half;
   // rotated pairs of q and k heads
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const float* __restrict__ C, i
     float v = 0.f;
     for (int s = 0; s < splits; ++s) v += cr[s * split_stride + c];
     const int h = e / hd, dd = e % hd;
-    st_from_f32<KV>(vbase + ((int64_t)h * g.page_tok + slot) * hd + dd, v);
+    st_from_f32<KV>(vbase + ((int64_t)h * hd + dd) * g.page_tok + slot, v);
   }
 }
 

@@ -11,15 +11,20 @@ struct KvGeom {
   int n_layers, n_kv, head_dim;
   int64_t page_elems;  // elements of one page across all layers
   int64_t layer_elems; // elements of one layer inside a page: 2 * n_kv * page_tok * head_dim
-  // K of (layer l, kv head h, slot j) at  page*page_elems + l*layer_elems + (h*page_tok + j)*head_dim
-  // V at the same offset + n_kv*page_tok*head_dim
+  // K of (layer l, kv head h, slot j, dim d) at  page*page_elems + l*layer_elems + (h*page_tok + j)*head_dim + d
+  // V (transposed) at  page*page_elems + l*layer_elems + n_kv*page_tok*head_dim + (h*head_dim + d)*page_tok + j
 };
 
 // dtype: 0 = fp32 storage, 1 = bf16 storage.  Activation operands (`act`,
 // `a_plane`) follow ActOut in rg_device.h: fp32 for fp32 models, hi/lo bf16
 // planes a_plane elements apart for bf16 models.
 
-// C[s][m][n] = sum_{k in split s} A[m][k] * W[n][k], fp32 output.
+// Output tile rows / columns launch_gemm uses for a given row bound.
+int gemm_tile_rows(int dtype, int rows_ub);
+int gemm_tile_cols(int dtype, int rows_ub);
+
+// C[s][m][n] = sum_{k in split s} A[m][k] * W[n][k], fp32 output.  bf16:
+// K and k_per_split multiples of 64, N a multiple of 16.
 hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, float* C, int ldc,
                        int64_t split_stride, const int* d_rows, int rows_ub, int N, int K, int splits,
                        int k_per_split, hipStream_t st);

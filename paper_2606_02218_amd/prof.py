@@ -1,0 +1,62 @@
+"""Summaries of rocprofv3 CSV output (kernel stats and counter collection).
+
+    python -m paper_2606_02218_amd.prof stats DIR              # per-kernel time table
+    python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import glob
+import os
+import re
+import sys
+
+
+def _find(d: str, suffix: str):
+    return sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+
+
+def _short(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "")
+    return re.sub(r"^void ", "", name)[:100]
+
+
+def stats_table(d: str) -> str:
+    rows = []
+    for f in _find(d, "kernel_stats.csv"):
+        rows += list(csv.DictReader(open(f)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    out = [f"{'kernel':100s} {'calls':>9s} {'total_ms':>10s} {'avg_us':>9s} {'pct':>6s}"]
+    for r in rows:
+        out.append(f"{_short(r['Name']):100s} {int(r['Calls']):9d} {float(r['TotalDurationNs']) / 1e6:10.1f} "
+                   f"{float(r['AverageNs']) / 1e3:9.2f} {float(r['Percentage']):6.2f}")
+    return "\n".join(out)
+
+
+def counter_table(d: str, regex: str) -> str:
+    pat = re.compile(regex)
+    acc = collections.defaultdict(lambda: [0, 0.0])
+    for f in _find(d, "counter_collection.csv"):
+        for r in csv.DictReader(open(f)):
+            name = r.get("Kernel_Name", "")
+            if not pat.search(name):
+                continue
+            key = (_short(name), r.get("Counter_Name", "?"))
+            a = acc[key]
+            a[0] += 1
+            a[1] += float(r.get("Counter_Value", 0) or 0)
+    out = [f"{'kernel':100s} {'counter':>12s} {'dispatches':>10s} {'mean_per_dispatch':>18s}"]
+    for (k, c), (n, v) in sorted(acc.items()):
+        out.append(f"{k:100s} {c:>12s} {n:10d} {v / max(1, n):18.1f}")
+    return "\n".join(out)
+
+
+if __name__ == "__main__":
+    if len(sys.argv) >= 3 and sys.argv[1] == "stats":
+        print(stats_table(sys.argv[2]))
+    elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
+        print(counter_table(sys.argv[2], sys.argv[3]))
+    else:
+        print(__doc__)
+        sys.exit(2)
