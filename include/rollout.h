@@ -53,10 +53,10 @@ extern "C" {
  * tokens are at positions 0..Lp-1, generated token t at Lp+t.  Query head h
  * reads key/value head floor(h*n_kv_heads/n_q_heads).  MLP =
  * W_down(silu(W_gate x) * (W_up x)).
- * Supported: head_dim a multiple of 8 and <= 256 (bf16 models: 64, 128 or
- * 256), n_q_heads a multiple of n_kv_heads with at most 8 query heads per kv
- * head, d_model, n_q_heads*head_dim and ffn_dim multiples of 64, vocab a
- * multiple of 16 (otherwise RG_EUNSUPPORTED). */
+ * Supported: head_dim 32, 64 or 128 (bf16 models: 64 or 128), n_q_heads a
+ * multiple of n_kv_heads with at most 8 query heads per kv head, d_model,
+ * n_q_heads*head_dim and ffn_dim multiples of 64, vocab a multiple of 16
+ * (otherwise RG_EUNSUPPORTED). */
 typedef struct rg_config {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
   int32_t eos_id;       /* token that ends a completion, in [0, vocab)                   */

@@ -40,7 +40,7 @@ int fail(int code, const std::string& msg) {
 
 constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
 constexpr int RG_SPLIT_MAX = 32;       // largest split-K factor of a decode GEMM
-constexpr int RG_GEMM_TARGET = 1024;   // blocks a GEMM launch aims for
+constexpr int RG_GEMM_TARGET = 512;    // blocks a GEMM launch aims for
 constexpr int RG_ATT_TARGET = 4096;    // work items an attention launch aims for
 constexpr int RG_RING = 64;            // async active-count slots
 constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
@@ -71,7 +71,8 @@ struct rg_policy {
   int64_t pool_pages = 0;
 
   float* x = nullptr;
-  void* abuf = nullptr;
+  void* abuf = nullptr;   // activation operand (ping)
+  void* abuf2 = nullptr;  // activation operand (pong)
   int64_t a_plane = 0;   // elements between the hi and lo planes of abuf (bf16 models)
   float* cpart = nullptr;
   int64_t cpart_elems = 0;
@@ -167,16 +168,17 @@ struct ProfScope {
     if (e_ != hipSuccess) return fail(RG_EHIP, std::string("launch ") + #kind + ": " + hipGetErrorString(e_)); \
   } while (0)
 
-// Split-K factor of a projection: enough blocks to cover the chip, each split
-// at least two 64-wide K steps, and split partials (written and read back as
-// fp32) no more than the weight bytes (S * rows * 4 <= K).
+// Split-K factor of a projection: enough blocks to cover the chip, each
+// split at least two 64-wide K steps, and the fp32 split partials (written
+// once, read once by the reducing block) within max(2 x weight bytes, 32 MB).
 void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits, int* kps) {
   int S = 1;
   if (pol->dtype == RG_DTYPE_BF16) {
     const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub), bn = gemm_tile_cols(pol->dtype, rows_ub);
     const int64_t blocks = ceil_div(N, bn) * ceil_div(rows_ub, bm);
     if (blocks < RG_GEMM_TARGET) S = (int)ceil_div(RG_GEMM_TARGET, blocks);
-    S = (int)std::min<int64_t>({(int64_t)S, K / 128, std::max<int64_t>(1, K / (4LL * rows_ub)), RG_SPLIT_MAX});
+    const int64_t budget = std::max<int64_t>(4LL * N * K, 32LL << 20);
+    S = (int)std::min<int64_t>({(int64_t)S, K / 128, budget / (4LL * rows_ub * N), RG_SPLIT_MAX});
     S = std::max(1, S);
   }
   const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
@@ -185,85 +187,92 @@ void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits,
   *splits = (int)ceil_div(K, k);
 }
 
-int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const void* W, int N, float* C,
-         const int* d_rows, int rows_ub, int* splits_out, int64_t* stride_out) {
-  int S, kps;
-  if (C == pol->cpart) {
-    choose_splits(pol, N, rows_ub, K, &S, &kps);
-    const int64_t fit = pol->cpart_elems / ((int64_t)rows_ub * N);   // splits the workspace holds
-    if (S > fit) {
-      const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
-      S = (int)std::max<int64_t>(1, fit);
-      kps = (int)ceil_div(ceil_div(K, S), step) * step;
-      S = (int)ceil_div(K, kps);
-    }
-  } else {   // direct output (the lm head into the logits buffer): never split
-    S = 1;
-    kps = K;
+// Split plan of a projection into the split-K workspace.
+void plan(const rg_policy* pol, int N, int rows_ub, int K, int* S, int* kps) {
+  choose_splits(pol, N, rows_ub, K, S, kps);
+  const int64_t fit = pol->cpart_elems / ((int64_t)rows_ub * N);   // splits the workspace holds
+  if (*S > fit) {
+    const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
+    *S = (int)std::max<int64_t>(1, fit);
+    *kps = (int)ceil_div(ceil_div(K, *S), step) * step;
+    *S = (int)ceil_div(K, *kps);
   }
-  const int64_t stride = (int64_t)rows_ub * N;
-  if (C == pol->cpart && stride * S > pol->cpart_elems)
-    return fail(RG_ENOMEM, "GEMM workspace too small");
-  LAUNCH(kind, launch_gemm(pol->dtype, A, K, pol->a_plane, W, K, C, N, stride, d_rows, rows_ub, N, K, S, kps, st));
-  if (splits_out) *splits_out = S;
-  if (stride_out) *stride_out = stride;
+}
+
+// One projection with its epilogue; the split plan and workspace are filled in here.
+int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const void* W, int N, const int* d_rows,
+         int rows_ub, GemmEpi ep, bool allow_split = true) {
+  int S = 1, kps = K;
+  if (allow_split) plan(pol, N, rows_ub, K, &S, &kps);
+  ep.part = pol->cpart;
+  ep.part_stride = (int64_t)rows_ub * N;
+  const bool needs_part = S > 1 || pol->dtype != RG_DTYPE_BF16;
+  if (needs_part && ep.part_stride * S > pol->cpart_elems) return fail(RG_ENOMEM, "GEMM workspace too small");
+  LAUNCH(kind, launch_gemm(pol->dtype, A, K, pol->a_plane, W, K, d_rows, rows_ub, N, K, S, kps, ep, st));
   return RG_OK;
 }
 
 // The decoder blocks over `rows_ub` rows (actual count at *d_rows), whose
-// row_tab / row_pos are set; ctx_max bounds every row's context length.
-int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max) {
+// row_tab / row_pos are set and whose first attention norm is in pol->abuf;
+// ctx_max bounds every row's context length.  On return pol->abuf holds the
+// final norm of every row (final_norm_rows) or x the residual stream after
+// the last block.
+int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max, bool final_norm_rows) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
   int n_chunks = 1;
   if ((int64_t)rows_ub * pol->nkv < RG_ATT_TARGET)
     n_chunks = (int)std::min<int64_t>(ceil_div(RG_ATT_TARGET, (int64_t)rows_ub * pol->nkv), ceil_div(ctx_max, 256));
-  n_chunks = std::max(1, n_chunks);
+  n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16384)});
   const int chunk_len = (int)ceil_div(ceil_div(ctx_max, n_chunks), 64) * 64;
   n_chunks = (int)ceil_div(ctx_max, chunk_len);
   if ((int64_t)rows_ub * n_chunks > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
+  const float eps = pol->cfg.rms_eps;
+  GemmEpi qkv{};
+  qkv.mode = GEMM_EPI_QKV;
+  qkv.q_out = pol->qbuf; qkv.kv_pool = pol->kv_pool; qkv.geom = pol->geom;
+  qkv.page_tab = pol->page_tab; qkv.tab_stride = tab_stride; qkv.row_tab = pol->row_tab; qkv.row_pos = pol->row_pos;
+  qkv.rope_cos = pol->rope_cos; qkv.rope_sin = pol->rope_sin; qkv.n_q = pol->nq; qkv.n_kv = pol->nkv; qkv.hd = pol->hd;
+  GemmEpi resid{};
+  resid.mode = GEMM_EPI_RESIDUAL; resid.x = pol->x; resid.ldx = pol->d;
+  GemmEpi swig{};
+  swig.mode = GEMM_EPI_SWIGLU; swig.act = ActOut{pol->abuf2, pol->a_plane}; swig.act_ld = pol->F;
+  int rc;
 
   for (int l = 0; l < pol->L; ++l) {
-    int S;
-    int64_t stride;
-    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[l], pol->d, pol->cfg.rms_eps, pol->abuf,
-                                         pol->a_plane, nullptr, d_rows, rows_ub, st));
-    int rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, pol->cpart, d_rows, rows_ub,
-                  &S, &stride);
-    if (rc) return rc;
-    LAUNCH(RG_K_QKV_ROPE, launch_qkv_rope(pol->dtype, pol->cpart, stride, S, pol->nq, pol->nkv, pol->hd,
-                                          pol->rope_cos, pol->rope_sin, pol->qbuf, pol->kv_pool, pol->geom, l,
-                                          pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, d_rows, rows_ub,
-                                          st));
+    qkv.layer = l;
+    if ((rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, d_rows, rows_ub, qkv)))
+      return rc;
     LAUNCH(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                        pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, chunk_len, n_chunks,
                                        pol->att_o, pol->att_ml, d_rows, rows_ub, st));
     LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
-                                              chunk_len, n_chunks, pol->abuf, pol->a_plane, d_rows, rows_ub, st));
-    rc = gemm(pol, st, RG_K_GEMM_O, pol->abuf, pol->q_dim, pol->w_o[l], pol->d, pol->cpart, d_rows, rows_ub, &S,
-              &stride);
-    if (rc) return rc;
-    LAUNCH(RG_K_RESIDUAL, launch_residual(pol->cpart, stride, S, pol->d, pol->x, d_rows, rows_ub, st));
-    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_ffn[l], pol->d, pol->cfg.rms_eps, pol->abuf,
-                                         pol->a_plane, nullptr, d_rows, rows_ub, st));
-    rc = gemm(pol, st, RG_K_GEMM_GU, pol->abuf, pol->d, pol->w_gu[l], 2 * pol->F, pol->cpart, d_rows, rows_ub, &S,
-              &stride);
-    if (rc) return rc;
-    LAUNCH(RG_K_SWIGLU, launch_swiglu(pol->dtype, pol->cpart, stride, S, pol->F, pol->abuf, pol->a_plane, d_rows, rows_ub, st));
-    rc = gemm(pol, st, RG_K_GEMM_DOWN, pol->abuf, pol->F, pol->w_down[l], pol->d, pol->cpart, d_rows, rows_ub, &S,
-              &stride);
-    if (rc) return rc;
-    LAUNCH(RG_K_RESIDUAL, launch_residual(pol->cpart, stride, S, pol->d, pol->x, d_rows, rows_ub, st));
+                                              chunk_len, n_chunks, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+    if ((rc = gemm(pol, st, RG_K_GEMM_O, pol->abuf2, pol->q_dim, pol->w_o[l], pol->d, d_rows, rows_ub, resid)))
+      return rc;
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_ffn[l], pol->d, eps, pol->abuf, pol->a_plane,
+                                         nullptr, d_rows, rows_ub, st));
+    if ((rc = gemm(pol, st, RG_K_GEMM_GU, pol->abuf, pol->d, pol->w_gu[l], 2 * pol->F, d_rows, rows_ub, swig)))
+      return rc;
+    if ((rc = gemm(pol, st, RG_K_GEMM_DOWN, pol->abuf2, pol->F, pol->w_down[l], pol->d, d_rows, rows_ub, resid)))
+      return rc;
+    const float* gnext = l + 1 < pol->L ? pol->g_attn[l + 1] : (final_norm_rows ? pol->w_final : nullptr);
+    if (gnext)
+      LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, gnext, pol->d, eps, pol->abuf, pol->a_plane, nullptr,
+                                           d_rows, rows_ub, st));
   }
   return RG_OK;
 }
 
-// Final norm + lm head for `rows_ub` rows into pol->logits.
+// The lm head into pol->logits.  src_rows != NULL (prefill): final norm of the
+// listed rows first; otherwise pol->abuf already holds the final norm.
 int run_head(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, const int32_t* src_rows) {
-  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->w_final, pol->d, pol->cfg.rms_eps, pol->abuf,
-                                       pol->a_plane, src_rows, d_rows, rows_ub, st));
-  return gemm(pol, st, RG_K_GEMM_LM, pol->abuf, pol->d, pol->w_lm, pol->V, pol->logits, d_rows, rows_ub, nullptr,
-              nullptr);
+  if (src_rows)
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->w_final, pol->d, pol->cfg.rms_eps, pol->abuf,
+                                         pol->a_plane, src_rows, d_rows, rows_ub, st));
+  GemmEpi store{};
+  store.mode = GEMM_EPI_STORE; store.C = pol->logits; store.ldc = pol->V;
+  return gemm(pol, st, RG_K_GEMM_LM, pol->abuf, pol->d, pol->w_lm, pol->V, d_rows, rows_ub, store, false);
 }
 
 int copy_weight(rg_policy* pol, void* dst, const void* src, size_t bytes, const char* what) {
@@ -287,8 +296,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       c.vocab < 2 || c.eos_id < 0 || c.eos_id >= c.vocab || !(c.rope_theta > 0.f) || !(c.rms_eps >= 0.f))
     return fail(RG_EINVAL, "rg_policy_create: invalid config");
   if (c.dtype != RG_DTYPE_F32 && c.dtype != RG_DTYPE_BF16) return fail(RG_EUNSUPPORTED, "unsupported dtype");
-  if (c.dtype == RG_DTYPE_BF16 && c.head_dim != 64 && c.head_dim != 128 && c.head_dim != 256)
-    return fail(RG_EUNSUPPORTED, "unsupported shape: bf16 models need head_dim 64, 128 or 256");
+  if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 128)
+    return fail(RG_EUNSUPPORTED, "unsupported shape: head_dim must be 32, 64 or 128 (bf16 models: 64 or 128)");
+  if (c.dtype == RG_DTYPE_BF16 && c.head_dim == 32)
+    return fail(RG_EUNSUPPORTED, "unsupported shape: bf16 models need head_dim 64 or 128");
   if (c.head_dim % 8 || c.head_dim > 256 || c.n_q_heads % c.n_kv_heads || c.n_q_heads / c.n_kv_heads > 8 ||
       c.d_model % 64 || (c.n_q_heads * c.head_dim) % 64 || c.ffn_dim % 64 || c.vocab % 16)
     return fail(RG_EUNSUPPORTED, "unsupported shape: need head_dim%8==0, head_dim<=256, n_q/n_kv integer <= 8, "
@@ -331,17 +342,38 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   for (int l = 0; l < pol->L; ++l) {
     void *qkv, *o, *gu, *dn;
     float *ga, *gf;
+    // [wq; wk; wv] with each head's rows reordered in 16-row tiles as dims
+    // (0-15, hd/2..hd/2+15, 16-31, hd/2+16.., ...): a rotated pair (d, d + hd/2)
+    // then sits in two adjacent 16-column tiles of the product
     if ((rc = pol->alloc(&qkv, (size_t)pol->qkv_n * d * eb))) return bail(rc);
-    char* q = (char*)qkv;
-    if ((rc = copy_weight(pol, q, w->wq[l], (size_t)pol->q_dim * d * eb, "wq"))) return bail(rc);
-    if ((rc = copy_weight(pol, q + (size_t)pol->q_dim * d * eb, w->wk[l], (size_t)pol->kv_dim * d * eb, "wk"))) return bail(rc);
-    if ((rc = copy_weight(pol, q + (size_t)(pol->q_dim + pol->kv_dim) * d * eb, w->wv[l], (size_t)pol->kv_dim * d * eb, "wv")))
-      return bail(rc);
+    if (!w->wq[l] || !w->wk[l] || !w->wv[l]) return bail(fail(RG_EINVAL, "weights: NULL wq/wk/wv"));
+    {
+      const int hd = pol->hd, half = hd / 2;
+      const size_t row = (size_t)d * eb;
+      const void* src[3] = {w->wq[l], w->wk[l], w->wv[l]};
+      const int heads[3] = {pol->nq, pol->nkv, pol->nkv};
+      size_t base = 0;
+      for (int part = 0; part < 3; ++part) {
+        for (int t = 0; t < hd / 16; ++t) {   // packed tile t of every head
+          const int d0 = (t & 1) ? half + (t >> 1) * 16 : (t >> 1) * 16;
+          HIPTRY(hipMemcpy2D((char*)qkv + (base + (size_t)t * 16) * row, (size_t)hd * row,
+                             (const char*)src[part] + (size_t)d0 * row, (size_t)hd * row, 16 * row, heads[part],
+                             hipMemcpyDeviceToDevice));
+        }
+        base += (size_t)heads[part] * hd;
+      }
+    }
     if ((rc = pol->alloc(&o, (size_t)d * pol->q_dim * eb))) return bail(rc);
     if ((rc = copy_weight(pol, o, w->wo[l], (size_t)d * pol->q_dim * eb, "wo"))) return bail(rc);
+    // gate/up interleaved in blocks of 16 rows: [gate 16b..16b+15 | up 16b..16b+15] for block b,
+    // so one 32-column tile of the product holds both halves of 16 SwiGLU outputs
     if ((rc = pol->alloc(&gu, (size_t)2 * pol->F * d * eb))) return bail(rc);
-    if ((rc = copy_weight(pol, gu, w->w_gate[l], (size_t)pol->F * d * eb, "w_gate"))) return bail(rc);
-    if ((rc = copy_weight(pol, (char*)gu + (size_t)pol->F * d * eb, w->w_up[l], (size_t)pol->F * d * eb, "w_up"))) return bail(rc);
+    if (!w->w_gate[l] || !w->w_up[l]) return bail(fail(RG_EINVAL, "weights: NULL w_gate/w_up"));
+    {
+      const size_t blk = (size_t)16 * d * eb;
+      HIPTRY(hipMemcpy2D(gu, 2 * blk, w->w_gate[l], blk, blk, pol->F / 16, hipMemcpyDeviceToDevice));
+      HIPTRY(hipMemcpy2D((char*)gu + blk, 2 * blk, w->w_up[l], blk, blk, pol->F / 16, hipMemcpyDeviceToDevice));
+    }
     if ((rc = pol->alloc(&dn, (size_t)d * pol->F * eb))) return bail(rc);
     if ((rc = copy_weight(pol, dn, w->w_down[l], (size_t)d * pol->F * eb, "w_down"))) return bail(rc);
     if ((rc = pol->alloc((void**)&ga, d * 4))) return bail(rc);
@@ -391,6 +423,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   std::vector<Piece> pieces = {
       {(void**)&pol->x, (size_t)(M * d * 4)},
       {&pol->abuf, (size_t)(M * kmax * 4)},   // fp32, or two bf16 planes
+      {&pol->abuf2, (size_t)(M * kmax * 4)},
       {(void**)&pol->cpart, (size_t)(pol->cpart_elems * 4)},
       {(void**)&pol->qbuf, (size_t)(M * pol->q_dim * 4)},
       {(void**)&pol->att_o, (size_t)(pol->att_rowchunks * pol->nq * pol->hd * 4)},
@@ -523,7 +556,9 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, Ni, pol->row_tab, pol->row_pos, (int)T_pre, st));
   LAUNCH(RG_K_EMBED, launch_embed(pol->dtype, pol->w_embed, pol->d, pol->V, prompts, pol->x, pol->state + 7, d_pre,
                                   (int)T_pre, st));
-  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen);
+  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                       pol->a_plane, nullptr, d_pre, (int)T_pre, st));
+  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen, false);
   if (rc) return rc;
   rc = run_head(pol, st, pol->state + 6, P, pol->last_rows);
   if (rc) return rc;
@@ -595,7 +630,9 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
     if (n_steps || oom) break;
     LAUNCH(RG_K_EMBED, launch_decode_rows(pol->dtype, pol->w_embed, pol->d, pol->act_seq, pol->act_tok, pol->seq_grp,
                                           pol->plen, t, pol->row_tab, pol->row_pos, pol->x, pol->state, m_ub, st));
-    if ((rc = run_layers(pol, st, pol->state, m_ub, max_plen + t))) return rc;
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                         pol->a_plane, nullptr, pol->state, m_ub, st));
+    if ((rc = run_layers(pol, st, pol->state, m_ub, max_plen + t, true))) return rc;
     if ((rc = run_head(pol, st, pol->state, m_ub, nullptr))) return rc;
     sm.t = t;
     LAUNCH(RG_K_SAMPLE, launch_sample(sm, m_ub, st));

@@ -9,10 +9,12 @@
 // bf16 KV: one wave per work item on MFMA 16x16x32.  Scores are formed
 // transposed, S^T = K Q^T (tokens x query heads), so each lane ends up holding
 // the probabilities of one query head for 8 tokens -- exactly a B fragment of
-// O^T = V^T P^T (the 8 tokens of a 32-token block are taken in the order the
-// S^T layout leaves them: 4g..4g+3 and 16+4g..16+4g+3 for lane group g, and
-// the V^T fragment is loaded in the same order).  q and p are fp32 values
-// split into hi/lo bf16 pairs, so both products keep fp32-level accuracy.
+// O^T = V^T P^T.  The K rows of each 16-token tile are permuted so that lane
+// group g ends up with the 8 consecutive tokens 8g..8g+7 of a 32-token block,
+// whose V^T fragment is one 16-byte load.  q and p are fp32 values split into
+// hi/lo bf16 pairs, so both products keep fp32-level accuracy.  The chunk's
+// page ids are read once into LDS and the next block's K and V are loaded
+// while the current block is multiplied.
 // fp32 KV (fp32 models): a plain per-token VALU kernel.
 #include "rg_device.h"
 #include "rg_kernels.h"
@@ -161,6 +163,40 @@ __device__ __forceinline__ void split8(const float* v, bf16x8_t& hi, bf16x8_t& l
   lo = __builtin_bit_cast(bf16x8_t, uint4{l[0], l[1], l[2], l[3]});
 }
 
+constexpr int ATT_MAX_CHUNK_PAGES = 1024;   // a chunk spans at most 16384 tokens
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// Registers of one 32-token block: K fragments of both 16-token tiles and the
+// V^T fragments of every 16-dim output tile.
+template <int HD>
+struct AttBlock {
+  u32x4_t k[2][HD / 32];
+  u32x4_t v[HD / 16];
+};
+
+template <int HD>
+__device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restrict__ pool, const KvGeom& g,
+                                         int64_t koff, int64_t voff, const int* spg, int c0, int c1, int t0,
+                                         int col, int grp) {
+  // K: A-fragment row i of tile tt is token t0 + 8*(i/4) + 4*tt + (i%4), so that
+  // the S^T layout leaves lane group grp holding tokens t0+8*grp .. +7
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    int tok = t0 + 8 * (col >> 2) + 4 * tt + (col & 3);
+    if (tok >= c1) tok = c0;                 // keep the load in bounds; masked later
+    const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff + (int64_t)(tok & 15) * HD + 8 * grp;
+#pragma unroll
+    for (int kb = 0; kb < HD / 32; ++kb) b.k[tt][kb] = *reinterpret_cast<const u32x4_t*>(kp + kb * 32);
+  }
+  // V^T: lane reads dims (dt*16 + col), tokens t0+8*grp .. +7 (one page slot run)
+  const int tv = t0 + 8 * grp;
+  const int pg = spg[((tv < c1 ? tv : c0) - c0) >> 4];
+  const bf16_t* vp = pool + (int64_t)pg * g.page_elems + voff + (tv & 15);
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) b.v[dt] = *reinterpret_cast<const u32x4_t*>(vp + (int64_t)(dt * 16 + col) * 16);
+}
+
 template <int HD>
 __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
                                                        const bf16_t* __restrict__ pool, KvGeom g, int layer,
@@ -189,8 +225,15 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
   const int c1 = min(ctx, c0 + chunk_len);
   const int rep = n_q / n_kv;
   const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
-  const int PT = g.page_tok;   // 16
 
+  // page ids of the chunk, once
+  __shared__ int spg[ATT_MAX_CHUNK_PAGES];
+  {
+    const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride + (c0 >> 4);
+    const int npg = (c1 - c0 + 15) >> 4;
+    for (int i = lane; i < npg; i += 64) spg[i] = tab[i];
+    __syncthreads();
+  }
   // Q^T fragments: lane holds q[head col][kb*32 + 8*grp + 0..7], pre-scaled by 1/sqrt(hd)
   bf16x8_t qh[HD / 32], ql[HD / 32];
   {
@@ -204,40 +247,38 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
       split8(v, qh[kb], ql[kb]);
     }
   }
-  const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * PT * HD;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * PT * HD;
+  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x4_t oacc[HD / 16];
 #pragma unroll
   for (int i = 0; i < HD / 16; ++i) oacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  AttBlock<HD> cur, nxt;
+  att_load<HD>(cur, pool, g, koff, voff, spg, c0, c1, c0, col, grp);
   for (int t0 = c0; t0 < c1; t0 += 32) {
-    // ---- S^T for tokens t0..t0+31 (two 16-token tiles)
+    if (t0 + 32 < c1) att_load<HD>(nxt, pool, g, koff, voff, spg, c0, c1, t0 + 32, col, grp);   // next block in flight
+    // ---- S^T = K Q^T; lane holds tokens t0 + 8*grp + 4*tt + j of query head col
     f32x4_t s[2];
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
-      int tok = t0 + tt * 16 + col;
-      if (tok >= c1) tok = c0;                     // keep the load in bounds; masked below
-      const bf16_t* kp = pool + (int64_t)tab[tok / PT] * g.page_elems + koff + (int64_t)(tok % PT) * HD + 8 * grp;
       f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < HD / 32; ++kb) {
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kp + kb * 32));
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, cur.k[tt][kb]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[kb], acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[kb], acc, 0, 0, 0);
       }
       s[tt] = acc;
     }
-    // ---- online softmax for query head `col`: lane holds tokens t0 + tt*16 + 4*grp + j
+    const int nval = min(8, max(0, c1 - (t0 + 8 * grp)));   // valid tokens among this lane group's 8
     float mloc = -INFINITY;
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int tok = t0 + tt * 16 + 4 * grp + j;
-        if (tok >= c1) s[tt][j] = -INFINITY;
+        if (4 * tt + j >= nval) s[tt][j] = -INFINITY;
         mloc = fmaxf(mloc, s[tt][j]);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
@@ -262,33 +303,22 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
     for (int i = 0; i < HD / 16; ++i) oacc[i] *= alpha;
     bf16x8_t ph, pl;
     split8(p, ph, pl);
-    // ---- O^T += V^T P^T; V^T fragment rows = dims, k = the same 8 tokens
-    const int pg0 = tab[t0 / PT];
-    const int pg1 = (t0 + 16 < c1) ? tab[t0 / PT + 1] : pg0;
-    const int nval0 = min(4, max(0, c1 - (t0 + 4 * grp)));          // valid tokens among 4*grp..+3
-    const int nval1 = min(4, max(0, c1 - (t0 + 16 + 4 * grp)));
-    const bf16_t* v0 = pool + (int64_t)pg0 * g.page_elems + voff + 4 * grp;
-    const bf16_t* v1 = pool + (int64_t)pg1 * g.page_elems + voff + 4 * grp;
+    // ---- O^T += V^T P^T (k = this lane group's 8 tokens, in order)
 #pragma unroll
     for (int dt = 0; dt < HD / 16; ++dt) {
-      const int dim = dt * 16 + col;
-      uint2 a0 = *reinterpret_cast<const uint2*>(v0 + (int64_t)dim * PT);
-      uint2 a1 = *reinterpret_cast<const uint2*>(v1 + (int64_t)dim * PT);
-      // zero the slots of masked tokens (their memory may hold anything)
-      if (nval0 < 4) {
-        const uint64_t keep = nval0 == 0 ? 0ull : (~0ull >> (64 - 16 * nval0));
-        const uint64_t v = ((uint64_t)a0.y << 32 | a0.x) & keep;
-        a0 = uint2{(uint32_t)v, (uint32_t)(v >> 32)};
+      u32x4_t vv = cur.v[dt];
+      if (nval < 8) {   // zero the slots of masked tokens (their memory may hold anything)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int n2 = nval - 2 * e;   // valid tokens in this dword
+          vv[e] = n2 >= 2 ? vv[e] : (n2 == 1 ? (vv[e] & 0xFFFFu) : 0u);
+        }
       }
-      if (nval1 < 4) {
-        const uint64_t keep = nval1 == 0 ? 0ull : (~0ull >> (64 - 16 * nval1));
-        const uint64_t v = ((uint64_t)a1.y << 32 | a1.x) & keep;
-        a1 = uint2{(uint32_t)v, (uint32_t)(v >> 32)};
-      }
-      const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, uint4{a0.x, a0.y, a1.x, a1.y});
+      const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, vv);
       oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, oacc[dt], 0, 0, 0);
       oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, oacc[dt], 0, 0, 0);
     }
+    cur = nxt;
   }
   // ---- partials: lane holds O^T[dims dt*16 + 4*grp + j][head col]
   if (col < rep) {
@@ -341,7 +371,7 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
   dim3 grid(n_chunks, n_kv, rows_ub);
   if (dtype == 1) {
     // two 16-slot pages per 32-token block, blocks 32-aligned inside a chunk
-    if (g.page_tok != 16 || chunk_len % 32 != 0) return hipErrorInvalidValue;
+    if (g.page_tok != 16 || chunk_len % 32 != 0 || chunk_len > 16 * ATT_MAX_CHUNK_PAGES) return hipErrorInvalidValue;
     const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
@@ -350,7 +380,6 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;
-      case 256: RG_ATT_MFMA(256); break;
       default: return hipErrorInvalidValue;
     }
 #undef RG_ATT_MFMA

@@ -1,5 +1,14 @@
-// Matrix products C = A W^T for the rollout: activations A [rows, K] times
-// weights W [N, K] (both K-contiguous), fp32 results, optional split over K.
+// Matrix products of the decoder, y = x W^T with activations [rows, K] and
+// weights W [N, K] (both K-contiguous), each with a fused epilogue:
+//   STORE     C[r][n] = y                          (lm head logits)
+//   RESIDUAL  x[r][n] += y                         (O and down projections)
+//   SWIGLU    act[r][f] = silu(gate) * up          (gate/up projection; packed
+//             columns come as [16 gate | 16 up] per 32)
+//   QKV       RoPE on the query and key heads; q -> fp32 buffer, k and v ->
+//             the row's KV page (keys as [slot][dim], values as [dim][slot]).
+//             Within each head the packed weight rows come in 16-row tiles
+//             ordered (dims 0-15, dims h/2..h/2+15, dims 16-31, ...) so that
+//             a rotated pair (d, d + h/2) lies in adjacent column tiles.
 //
 // bf16 models: LDS-tiled gfx950 MFMA (v_mfma_f32_16x16x32_bf16).  A block
 // owns a BM x BN output tile and walks its K range in BK = 64 steps: every
@@ -8,8 +17,11 @@
 // the pieces are written to LDS for the next step.  Each wave owns a WM x WN
 // grid of 16 x 16 MFMA tiles.  The activation comes as hi/lo bf16 planes and
 // every fragment takes two MFMAs (W*hi + W*lo) into one fp32 accumulator.
-// Tile shapes are chosen by the row count: 16 rows for the decode tail up to
-// 256 x 128 tiles for prefill.
+//
+// Split over K: the grid's z dimension splits K and every split writes its
+// fp32 partial; k_split_epilogue then sums the partials in split order (one
+// block per row and 128 columns) and runs the epilogue.  Without a split the
+// epilogue runs straight from the accumulators.
 //
 // MFMA 16x16x32 lane layout: lane l supplies row (l % 16), k-slice
 // 8*(l / 16) .. +7 of A and column (l % 16), the same k-slice of B; it
@@ -29,16 +41,94 @@ __device__ __forceinline__ bf16x8_t lds_frag(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(p));
 }
 
-template <int BM, int BN, int WM, int WN>
+template <typename KV>
+__device__ __forceinline__ void kv_store(KV* p, float v);
+template <> __device__ __forceinline__ void kv_store<float>(float* p, float v) { *p = v; }
+template <> __device__ __forceinline__ void kv_store<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// Sum of the split partials of element (r, c), in split order.
+__device__ __forceinline__ float split_sum(const GemmEpi& ep, int S, int64_t off) {
+  float v = 0.f;
+  for (int s = 0; s < S; ++s) v += ep.part[s * ep.part_stride + off];
+  return v;
+}
+
+// QKV epilogue of row r for packed column c (a lower-half tile column: bit 4
+// of c is 0) holding dim d of its head, and c + 16 holding dim d + half.
+template <typename KV>
+__device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float a, float b) {
+  const int hd = ep.hd, half = hd / 2;
+  const int head = c / hd, p = c % hd;
+  const int d = (p >> 5) * 16 + (p & 15);
+  const int pos = ep.row_pos[r];
+  KV* pool = (KV*)ep.kv_pool;
+  if (head >= ep.n_q + ep.n_kv) {                     // value head: no rotation, V^T layout
+    const int kvh = head - ep.n_q - ep.n_kv;
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / ep.geom.page_tok];
+    KV* vb = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
+             ((int64_t)ep.n_kv + kvh) * ep.geom.page_tok * hd + pos % ep.geom.page_tok;
+    kv_store<KV>(vb + (int64_t)d * ep.geom.page_tok, a);
+    kv_store<KV>(vb + (int64_t)(d + half) * ep.geom.page_tok, b);
+    return;
+  }
+  const float co = ep.rope_cos[(int64_t)pos * half + d], si = ep.rope_sin[(int64_t)pos * half + d];
+  const float ra = a * co - b * si, rb = b * co + a * si;
+  if (head < ep.n_q) {
+    float* qo = ep.q_out + ((int64_t)r * ep.n_q + head) * hd;
+    qo[d] = ra;
+    qo[d + half] = rb;
+  } else {
+    const int kvh = head - ep.n_q;
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / ep.geom.page_tok];
+    KV* kp = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
+             ((int64_t)kvh * ep.geom.page_tok + pos % ep.geom.page_tok) * hd;
+    kv_store<KV>(kp + d, ra);
+    kv_store<KV>(kp + d + half, rb);
+  }
+}
+
+// Epilogue of a finished tile whose split partials are in ep.part: rows
+// m0..m0+BM-1 (< M), columns n0..n0+BN-1 (< N).  Every thread of the block
+// calls it.
+template <int EPI, int BM, int BN, int NT, int SPLIT, typename KV>
+__device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, int N, int tid) {
+  if constexpr (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_RESIDUAL) {
+    for (int i = tid; i < BM * BN; i += NT) {
+      const int r = m0 + i / BN, c = n0 + i % BN;
+      if (r >= M || c >= N) continue;
+      const float v = split_sum(ep, S, (int64_t)r * N + c);
+      if constexpr (EPI == GEMM_EPI_STORE) ep.C[(int64_t)r * ep.ldc + c] = v;
+      else ep.x[(int64_t)r * ep.ldx + c] += v;
+    }
+  } else if constexpr (EPI == GEMM_EPI_SWIGLU) {
+    for (int i = tid; i < BM * (BN / 2); i += NT) {
+      const int r = m0 + i / (BN / 2), q = i % (BN / 2);
+      const int gc = n0 + (q >> 4) * 32 + (q & 15);    // gate column; up is 16 further
+      if (r >= M || gc >= N) continue;
+      const float gt = split_sum(ep, S, (int64_t)r * N + gc);
+      const float up = split_sum(ep, S, (int64_t)r * N + gc + 16);
+      act_store<SPLIT>(ep.act, (int64_t)r * ep.act_ld + (gc >> 5) * 16 + (q & 15), gt / (1.0f + expf(-gt)) * up);
+    }
+  } else {  // GEMM_EPI_QKV: packed columns; a lower-half tile owns the rotated pair
+    for (int i = tid; i < BM * BN; i += NT) {
+      const int r = m0 + i / BN, c = n0 + i % BN;
+      if (r >= M || c >= N || ((c >> 4) & 1)) continue;
+      const int64_t roff = (int64_t)r * N;
+      qkv_store<KV>(ep, r, c, split_sum(ep, S, roff + c), split_sum(ep, S, roff + c + 16));
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
-    float* __restrict__ C, int ldc, int64_t split_stride, const int* __restrict__ d_rows, int N, int K,
-    int k_per_split) {
+    const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep) {
   constexpr int WAVES_M = BM / (16 * WM), WAVES_N = BN / (16 * WN);
   constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int A_PIECES = BM * (BK / 8);          // 16-byte pieces per A plane tile
   constexpr int W_PIECES = BN * (BK / 8);
   static_assert((2 * A_PIECES) % NT == 0 && W_PIECES % NT == 0, "tile pieces must split evenly over threads");
+  static_assert((EPI != GEMM_EPI_SWIGLU && EPI != GEMM_EPI_QKV) || WN % 2 == 0, "pairs of adjacent column tiles");
   constexpr int A_PER_T = 2 * A_PIECES / NT;
   constexpr int W_PER_T = W_PIECES / NT;
   __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LROW];
@@ -112,80 +202,160 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   }
 #undef RG_FETCH
 #undef RG_STASH
-  float* cp = C + blockIdx.z * split_stride;
+
+  if constexpr (EPI == GEMM_EPI_PARTIAL) {
+    float* pp = ep.part + blockIdx.z * ep.part_stride;
 #pragma unroll
-  for (int i = 0; i < WM; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-    for (int j = 0; j < WN; ++j) {
-      const int col = n0 + (wn * WN + j) * 16 + lr;
-      if (col >= N) continue;
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + (wn * WN + j) * 16 + lr;
+        if (col >= N) continue;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4 + e;
-        if (r < M) cp[(int64_t)r * ldc + col] = acc[i][j][e];
+        for (int e = 0; e < 4; ++e) {
+          const int r = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4 + e;
+          if (r < M) pp[(int64_t)r * N + col] = acc[i][j][e];
+        }
       }
-    }
+  } else if constexpr (EPI == GEMM_EPI_SWIGLU || EPI == GEMM_EPI_QKV) {
+    // tiles 2m and 2m+1 of a wave pair up: (gate, up) or (dims d, d + half)
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; j += 2) {
+        const int c = n0 + (wn * WN + j) * 16 + lr;   // lower tile's column
+        if (c >= N) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4 + e;
+          if (r >= M) continue;
+          const float a = acc[i][j][e], b = acc[i][j + 1][e];
+          if constexpr (EPI == GEMM_EPI_SWIGLU)
+            act_store<1>(ep.act, (int64_t)r * ep.act_ld + (c >> 5) * 16 + lr, a / (1.0f + expf(-a)) * b);
+          else
+            qkv_store<bf16_t>(ep, r, c, a, b);
+        }
+      }
+  } else {
+    float* cp = EPI == GEMM_EPI_RESIDUAL ? ep.x : ep.C;
+    const int ld = EPI == GEMM_EPI_RESIDUAL ? ep.ldx : ep.ldc;
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + (wn * WN + j) * 16 + lr;
+        if (col >= N) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4 + e;
+          if (r < M) {
+            if constexpr (EPI == GEMM_EPI_RESIDUAL) cp[(int64_t)r * ld + col] += acc[i][j][e];
+            else cp[(int64_t)r * ld + col] = acc[i][j][e];
+          }
+        }
+      }
+  }
 }
 
-// fp32 models: plain fp32 FMA, one thread per output, 64 columns x 4 rows per block.
+// Sum of split partials + epilogue: one block of 128 threads per (128
+// columns, row).  SPLIT: activation output as hi/lo bf16 planes.
+template <int EPI, int SPLIT, typename KV>
+__global__ __launch_bounds__(128) void k_split_epilogue(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+  const int r = blockIdx.y;
+  if (r >= *d_rows) return;
+  tile_epilogue<EPI, 1, 128, 128, SPLIT, KV>(ep, S, r, blockIdx.x * 128, r + 1, N, threadIdx.x);
+}
+
+// fp32 models: plain fp32 FMA, one thread per output, 64 columns x 4 rows per
+// block, into the partial buffer; k_split_epilogue then runs the epilogue.
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, int lda,
                                                   const float* __restrict__ W, int ldw,
-                                                  float* __restrict__ C, int ldc, int64_t split_stride,
-                                                  const int* __restrict__ d_rows, int N, int K,
-                                                  int k_per_split) {
+                                                  float* __restrict__ C, const int* __restrict__ d_rows, int N,
+                                                  int K) {
   const int M = *d_rows;
   const int r = blockIdx.y * 4 + (threadIdx.x >> 6);
   const int n = blockIdx.x * 64 + (threadIdx.x & 63);
   if (r >= M || n >= N) return;
-  const int kb = blockIdx.z * k_per_split;
-  const int ke = min(K, kb + k_per_split);
   const float* a = A + (int64_t)r * lda;
   const float* w = W + (int64_t)n * ldw;
   float acc = 0.f;
-  for (int k = kb; k < ke; ++k) acc = fmaf(a[k], w[k], acc);
-  C[blockIdx.z * split_stride + (int64_t)r * ldc + n] = acc;
+  for (int k = 0; k < K; ++k) acc = fmaf(a[k], w[k], acc);
+  C[(int64_t)r * N + n] = acc;
 }
 
 template <int BM, int BN, int WM, int WN>
-hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, int ldw, float* C, int ldc,
-                        int64_t split_stride, const int* d_rows, int rows_ub, int N, int K, int splits,
-                        int k_per_split, hipStream_t st) {
+hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
+                        int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   constexpr int NT = (BM / (16 * WM)) * (BN / (16 * WN)) * 64;
   dim3 grid((N + BN - 1) / BN, (rows_ub + BM - 1) / BM, splits);
-  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane,
-                     (const bf16_t*)W, ldw, C, ldc, split_stride, d_rows, N, K, k_per_split);
+#define RG_TILED(E)                                                                                           \
+  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, E>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane, \
+                     (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep)
+  if (splits > 1) {
+    RG_TILED(GEMM_EPI_PARTIAL);
+  } else {
+    switch (ep.mode) {
+      case GEMM_EPI_STORE: RG_TILED(GEMM_EPI_STORE); break;
+      case GEMM_EPI_RESIDUAL: RG_TILED(GEMM_EPI_RESIDUAL); break;
+      case GEMM_EPI_SWIGLU: RG_TILED(GEMM_EPI_SWIGLU); break;
+      case GEMM_EPI_QKV: RG_TILED(GEMM_EPI_QKV); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+#undef RG_TILED
+  return hipGetLastError();
+}
+
+template <int SPLIT, typename KV>
+hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, const GemmEpi& ep, hipStream_t st) {
+  dim3 grid((N + 127) / 128, rows_ub);
+  switch (ep.mode) {
+    case GEMM_EPI_STORE: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_STORE, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
+    case GEMM_EPI_RESIDUAL: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_RESIDUAL, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
+    case GEMM_EPI_SWIGLU: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_SWIGLU, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
+    case GEMM_EPI_QKV: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_QKV, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 }  // namespace
 
 int gemm_tile_rows(int dtype, int rows_ub) {
-  if (dtype != 1) return 4;
+  if (dtype != 1) return 16;
   if (rows_ub <= 16) return 16;
   if (rows_ub <= 32) return 32;
   if (rows_ub <= 64) return 64;
-  if (rows_ub <= 128) return 128;
+  if (rows_ub <= 1024) return 128;
   return 256;
 }
 
-int gemm_tile_cols(int dtype, int rows_ub) { return dtype == 1 ? 128 : 64; }
+int gemm_tile_cols(int dtype, int rows_ub) { return 128; }
 
-hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, float* C, int ldc,
-                       int64_t split_stride, const int* d_rows, int rows_ub, int N, int K, int splits,
-                       int k_per_split, hipStream_t st) {
+hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
+                       int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
+  if ((splits > 1 || dtype != 1) && !ep.part) return hipErrorInvalidValue;
+  if ((ep.mode == GEMM_EPI_SWIGLU || ep.mode == GEMM_EPI_QKV) && N % 32) return hipErrorInvalidValue;
+  if (ep.mode == GEMM_EPI_QKV && (ep.hd % 32 || 128 % ep.hd)) return hipErrorInvalidValue;
+  hipError_t e;
   if (dtype == 1) {
     if (K % BK || k_per_split % BK || N % 16) return hipErrorInvalidValue;
     switch (gemm_tile_rows(dtype, rows_ub)) {
-      case 16: return launch_tiled<16, 128, 1, 2>(A, lda, a_plane, W, ldw, C, ldc, split_stride, d_rows, rows_ub, N, K, splits, k_per_split, st);
-      case 32: return launch_tiled<32, 128, 1, 4>(A, lda, a_plane, W, ldw, C, ldc, split_stride, d_rows, rows_ub, N, K, splits, k_per_split, st);
-      case 64: return launch_tiled<64, 128, 2, 4>(A, lda, a_plane, W, ldw, C, ldc, split_stride, d_rows, rows_ub, N, K, splits, k_per_split, st);
-      case 128: return launch_tiled<128, 128, 4, 4>(A, lda, a_plane, W, ldw, C, ldc, split_stride, d_rows, rows_ub, N, K, splits, k_per_split, st);
-      default: return launch_tiled<256, 128, 4, 4>(A, lda, a_plane, W, ldw, C, ldc, split_stride, d_rows, rows_ub, N, K, splits, k_per_split, st);
+      case 16: e = launch_tiled<16, 128, 1, 2>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 32: e = launch_tiled<32, 128, 1, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 64: e = launch_tiled<64, 128, 2, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 128: e = launch_tiled<128, 128, 4, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      default: e = launch_tiled<256, 128, 4, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
     }
+    if (e != hipSuccess || splits == 1) return e;
+    return launch_split_epilogue<1, bf16_t>(d_rows, rows_ub, N, splits, ep, st);
   }
-  dim3 grid((N + 63) / 64, (rows_ub + 3) / 4, splits);
-  hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, st, (const float*)A, lda, (const float*)W, ldw, C, ldc,
-                     split_stride, d_rows, N, K, k_per_split);
-  return hipGetLastError();
+  // fp32: whole-K product into the partial buffer, then the epilogue
+  if (splits != 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gemm_f32, dim3((N + 63) / 64, (rows_ub + 3) / 4), dim3(256), 0, st, (const float*)A, lda,
+                     (const float*)W, ldw, ep.part, d_rows, N, K);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_split_epilogue<0, float>(d_rows, rows_ub, N, 1, ep, st);
 }

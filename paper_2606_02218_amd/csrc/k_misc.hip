@@ -1,6 +1,5 @@
 // Row-wise kernels of the decoder step: embedding gather and row set-up,
-// RMSNorm, the fused QKV epilogue (split-K sum, RoPE, KV append), residual
-// add, SwiGLU, page copies, plus the Philox test hooks.
+// RMSNorm, residual add, page copies, plus the Philox test hooks.
 #include "rg_device.h"
 #include "rg_kernels.h"
 
@@ -64,60 +63,6 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, co
   for (int i = threadIdx.x; i < d; i += blockDim.x) act_store<SPLIT>(out, (int64_t)r * d + i, xr[i] * inv * g[i]);
 }
 
-template <typename KV>
-__global__ __launch_bounds__(256) void k_qkv_rope(const float* __restrict__ C, int64_t split_stride, int splits,
-                                                  int n_q, int n_kv, int hd, const float* __restrict__ rope_cos,
-                                                  const float* __restrict__ rope_sin, float* __restrict__ q_out,
-                                                  KV* __restrict__ pool, KvGeom g, int layer,
-                                                  const int32_t* __restrict__ page_tab, int tab_stride,
-                                                  const int32_t* __restrict__ row_tab,
-                                                  const int32_t* __restrict__ row_pos,
-                                                  const int* __restrict__ d_rows) {
-  const int r = blockIdx.x;
-  if (r >= *d_rows) return;
-  const int half = hd / 2;
-  const int ncols = (n_q + 2 * n_kv) * hd;
-  const float* cr = C + (int64_t)r * ncols;
-  const int pos = row_pos[r];
-  const int page = page_tab[(int64_t)row_tab[r] * tab_stride + pos / g.page_tok];
-  const int slot = pos % g.page_tok;
-  KV* kbase = pool + (int64_t)page * g.page_elems + (int64_t)layer * g.layer_elems;   // K [head][slot][dim]
-  KV* vbase = kbase + (int64_t)n_kv * g.page_tok * hd;                                 // V^T [head][dim][slot]
-  const float* cs = rope_cos + (int64_t)pos * half;
-  const float* sn = rope_sin + (int64_t)pos * half;
-  // rotated pairs of q and k heads
-  const int n_pairs = (n_q + n_kv) * half;
-  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
-    const int head = p / half, i = p % half;
-    const int c = head * hd + i;
-    float a = 0.f, b = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      a += cr[s * split_stride + c];
-      b += cr[s * split_stride + c + half];
-    }
-    const float co = cs[i], si = sn[i];
-    const float ra = a * co - b * si, rb = b * co + a * si;
-    if (head < n_q) {
-      float* qo = q_out + ((int64_t)r * n_q + head) * hd;
-      qo[i] = ra;
-      qo[i + half] = rb;
-    } else {
-      KV* kp = kbase + ((int64_t)(head - n_q) * g.page_tok + slot) * hd;
-      st_from_f32<KV>(kp + i, ra);
-      st_from_f32<KV>(kp + i + half, rb);
-    }
-  }
-  // values
-  const int nv = n_kv * hd;
-  for (int e = threadIdx.x; e < nv; e += blockDim.x) {
-    const int c = (n_q + n_kv) * hd + e;
-    float v = 0.f;
-    for (int s = 0; s < splits; ++s) v += cr[s * split_stride + c];
-    const int h = e / hd, dd = e % hd;
-    st_from_f32<KV>(vbase + ((int64_t)h * hd + dd) * g.page_tok + slot, v);
-  }
-}
-
 __global__ void k_residual(const float* __restrict__ C, int64_t split_stride, int splits, int N, float* __restrict__ x,
                            const int* __restrict__ d_rows) {
   const int r = blockIdx.y;
@@ -128,23 +73,6 @@ __global__ void k_residual(const float* __restrict__ C, int64_t split_stride, in
   float v = 0.f;
   for (int s = 0; s < splits; ++s) v += C[s * split_stride + o];
   x[o] += v;
-}
-
-template <int SPLIT>
-__global__ void k_swiglu(const float* __restrict__ C, int64_t split_stride, int splits, int F, ActOut out,
-                         const int* __restrict__ d_rows) {
-  const int r = blockIdx.y;
-  if (r >= *d_rows) return;
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= F) return;
-  const int64_t o = (int64_t)r * 2 * F + j;
-  float gt = 0.f, up = 0.f;
-  for (int s = 0; s < splits; ++s) {
-    gt += C[s * split_stride + o];
-    up += C[s * split_stride + o + F];
-  }
-  const float silu = gt / (1.0f + expf(-gt));
-  act_store<SPLIT>(out, (int64_t)r * F + j, silu * up);
 }
 
 template <typename KV>
@@ -234,39 +162,17 @@ hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, floa
   return hipGetLastError();
 }
 
-hipError_t launch_qkv_rope(int dtype, const float* C, int64_t split_stride, int splits, int n_q, int n_kv,
-                           int head_dim, const float* rope_cos, const float* rope_sin, float* q_out, void* kv_pool,
-                           KvGeom g, int layer, const int32_t* page_tab, int tab_stride, const int32_t* row_tab,
-                           const int32_t* row_pos, const int* d_rows, int rows_ub, hipStream_t st) {
+hipError_t launch_residual_norm(int dtype, const float* C, int64_t split_stride, int splits, int N, float* x,
+                                const float* g, float eps, void* out, int64_t a_plane, const int* d_rows,
+                                int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_qkv_rope<bf16_t>, dim3(rows_ub), dim3(256), 0, st, C, split_stride, splits, n_q, n_kv, head_dim,
-                       rope_cos, rope_sin, q_out, (bf16_t*)kv_pool, g, layer, page_tab, tab_stride, row_tab, row_pos,
+  if (C) {
+    hipLaunchKernelGGL(k_residual, dim3((N + 255) / 256, rows_ub), dim3(256), 0, st, C, split_stride, splits, N, x,
                        d_rows);
-  else
-    hipLaunchKernelGGL(k_qkv_rope<float>, dim3(rows_ub), dim3(256), 0, st, C, split_stride, splits, n_q, n_kv, head_dim,
-                       rope_cos, rope_sin, q_out, (float*)kv_pool, g, layer, page_tab, tab_stride, row_tab, row_pos,
-                       d_rows);
-  return hipGetLastError();
-}
-
-hipError_t launch_residual(const float* C, int64_t split_stride, int splits, int N, float* x, const int* d_rows,
-                           int rows_ub, hipStream_t st) {
-  if (rows_ub <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_residual, dim3((N + 255) / 256, rows_ub), dim3(256), 0, st, C, split_stride, splits, N, x, d_rows);
-  return hipGetLastError();
-}
-
-hipError_t launch_swiglu(int dtype, const float* C, int64_t split_stride, int splits, int F, void* out,
-                         int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st) {
-  if (rows_ub <= 0) return hipSuccess;
-  dim3 grid((F + 255) / 256, rows_ub);
-  const ActOut o{out, a_plane};
-  if (dtype == 1)
-    hipLaunchKernelGGL(k_swiglu<1>, grid, dim3(256), 0, st, C, split_stride, splits, F, o, d_rows);
-  else
-    hipLaunchKernelGGL(k_swiglu<0>, grid, dim3(256), 0, st, C, split_stride, splits, F, o, d_rows);
-  return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !g) return e;
+  }
+  return launch_rmsnorm(dtype, x, g, N, eps, out, a_plane, nullptr, d_rows, rows_ub, st);
 }
 
 hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs, int max_pairs,

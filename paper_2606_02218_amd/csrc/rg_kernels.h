@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rg_device.h"
+
 struct KvGeom {
   int page_tok;        // tokens per page
   int n_layers, n_kv, head_dim;
@@ -23,11 +25,28 @@ struct KvGeom {
 int gemm_tile_rows(int dtype, int rows_ub);
 int gemm_tile_cols(int dtype, int rows_ub);
 
-// C[s][m][n] = sum_{k in split s} A[m][k] * W[n][k], fp32 output.  bf16:
-// K and k_per_split multiples of 64, N a multiple of 16.
-hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, float* C, int ldc,
-                       int64_t split_stride, const int* d_rows, int rows_ub, int N, int K, int splits,
-                       int k_per_split, hipStream_t st);
+// Epilogue of a projection (see k_gemm.hip).
+enum { GEMM_EPI_STORE = 0,      // C[r][n] = y
+       GEMM_EPI_RESIDUAL = 1,   // x[r][n] += y
+       GEMM_EPI_SWIGLU = 2,     // columns packed [16 gate | 16 up] per 32; act[r][f] = silu(g) * u
+       GEMM_EPI_QKV = 3,        // RoPE; q -> q_out, k and v -> the row's KV page
+       GEMM_EPI_PARTIAL = 4 };  // (internal) split partial to part[s]
+struct GemmEpi {
+  int mode;
+  float* C; int ldc;                      // STORE
+  float* x; int ldx;                      // RESIDUAL
+  ActOut act; int act_ld;                 // SWIGLU
+  float* q_out; void* kv_pool; KvGeom geom; int layer;      // QKV
+  const int32_t* page_tab; int tab_stride; const int32_t* row_tab; const int32_t* row_pos;
+  const float* rope_cos; const float* rope_sin; int n_q, n_kv, hd;
+  float* part; int64_t part_stride;       // split partials [S][rows][N] (S > 1 and fp32 models)
+};
+
+// y = A W^T over rows < *d_rows with K split `splits` ways (bf16 models: K
+// and k_per_split multiples of 64, N a multiple of 16; fp32 models: one
+// split), then the epilogue ep.
+hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
+                       int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st);
 
 // x[r] = embed[tok[r]] (fp32), r < *d_rows.  Prefill: tok = prompts.  An id
 // outside [0, V) reads row 0 instead and sets *bad_token = 1.
@@ -52,14 +71,6 @@ hipError_t launch_prefill_rows(const int32_t* prompt_off, int P, int tab_base, i
 hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, float eps, void* out, int64_t a_plane,
                           const int32_t* src_rows, const int* d_rows, int rows_ub, hipStream_t st);
 
-// Sum the GEMM splits of the fused QKV product, rotate q and k, write q (fp32)
-// and append k, v to the row's KV page.
-hipError_t launch_qkv_rope(int dtype, const float* C, int64_t split_stride, int splits, int n_q,
-                           int n_kv, int head_dim, const float* rope_cos, const float* rope_sin,
-                           float* q_out, void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
-                           int tab_stride, const int32_t* row_tab, const int32_t* row_pos,
-                           const int* d_rows, int rows_ub, hipStream_t st);
-
 // Paged causal attention.  Row r's context is positions 0..row_pos[r] of page
 // table row_tab[r]; it is split into n_chunks chunks of chunk_len tokens
 // (a multiple of 256); each (row, kv head, chunk) block writes a partial
@@ -76,14 +87,12 @@ hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_m
                              int head_dim, const int32_t* row_pos, int chunk_len, int n_chunks, void* out,
                              int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
 
-// x[r][n] += sum_s C[s][r][n]
-hipError_t launch_residual(const float* C, int64_t split_stride, int splits, int N, float* x,
-                           const int* d_rows, int rows_ub, hipStream_t st);
-
-// out[r][j] = silu(g) * u with g = sum_s C[s][r][j], u = sum_s C[s][r][F + j],
-// as an activation operand.
-hipError_t launch_swiglu(int dtype, const float* C, int64_t split_stride, int splits, int F, void* out,
-                         int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
+// x[r][n] += sum_s C[s][r][n] (C may be NULL: no add; one block per 256
+// columns of a row), then, if g != NULL, out[r] = x[r] / sqrt(mean(x[r]^2) +
+// eps) * g as an activation operand (one block per row).
+hipError_t launch_residual_norm(int dtype, const float* C, int64_t split_stride, int splits, int N, float* x,
+                                const float* g, float eps, void* out, int64_t a_plane, const int* d_rows,
+                                int rows_ub, hipStream_t st);
 
 struct SampleArgs {
   const float* logits;      // [rows][V] or [P][V] when logits_by_group

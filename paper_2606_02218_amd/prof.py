@@ -1,6 +1,7 @@
 """Summaries of rocprofv3 CSV output (kernel stats and counter collection).
 
     python -m paper_2606_02218_amd.prof stats DIR              # per-kernel time table
+    python -m paper_2606_02218_amd.prof trace DIR [TOP]        # per kernel and grid size, from kernel_trace.csv
     python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
 """
 from __future__ import annotations
@@ -34,6 +35,30 @@ def stats_table(d: str) -> str:
     return "\n".join(out)
 
 
+def trace_table(d: str, top: int = 60) -> str:
+    """Dispatch time grouped by (kernel, grid size): the grid of the row-sized
+    kernels tells the row bucket of a decode step."""
+    acc = collections.defaultdict(lambda: [0, 0.0])
+    span = [None, None]
+    for f in _find(d, "kernel_trace.csv"):
+        for r in csv.DictReader(open(f)):
+            s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+            span[0] = s0 if span[0] is None else min(span[0], s0)
+            span[1] = e0 if span[1] is None else max(span[1], e0)
+            grid = "x".join(r.get(k, "") for k in ("Grid_Size_X", "Grid_Size_Y", "Grid_Size_Z"))
+            wg = "x".join(r.get(k, "") for k in ("Workgroup_Size_X", "Workgroup_Size_Y", "Workgroup_Size_Z"))
+            name = _short(r.get("Kernel_Name", "?")).split("(")[0]
+            a = acc[(name, grid, wg)]
+            a[0] += 1
+            a[1] += (e0 - s0) / 1e3
+    tot = sum(v[1] for v in acc.values())
+    out = [f"span_ms {((span[1] or 0) - (span[0] or 0)) / 1e6:.1f}  busy_ms {tot / 1e3:.1f}",
+           f"{'kernel':44s} {'grid':>22s} {'wg':>10s} {'calls':>8s} {'total_ms':>10s} {'avg_us':>9s}"]
+    for (k, g, w), (n, us) in sorted(acc.items(), key=lambda kv: -kv[1][1])[:top]:
+        out.append(f"{k[:44]:44s} {g:>22s} {w:>10s} {n:8d} {us / 1e3:10.1f} {us / n:9.2f}")
+    return "\n".join(out)
+
+
 def counter_table(d: str, regex: str) -> str:
     pat = re.compile(regex)
     acc = collections.defaultdict(lambda: [0, 0.0])
@@ -55,6 +80,8 @@ def counter_table(d: str, regex: str) -> str:
 if __name__ == "__main__":
     if len(sys.argv) >= 3 and sys.argv[1] == "stats":
         print(stats_table(sys.argv[2]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "trace":
+        print(trace_table(sys.argv[2], int(sys.argv[3]) if len(sys.argv) > 3 else 60))
     elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
         print(counter_table(sys.argv[2], sys.argv[3]))
     else:
