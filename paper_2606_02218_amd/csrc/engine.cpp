@@ -16,6 +16,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -39,12 +40,13 @@ int fail(int code, const std::string& msg) {
   } while (0)
 
 constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
-constexpr int RG_SPLIT_MAX = 32;       // largest split-K factor of a decode GEMM
+constexpr int RG_SPLIT_MAX = GEMM_MAX_SPLITS;   // largest split-K factor of a decode GEMM
 constexpr int RG_GEMM_TARGET = 512;    // blocks a GEMM launch aims for
 constexpr int RG_ATT_TARGET = 4096;    // work items an attention launch aims for
 constexpr int RG_RING = 64;            // async active-count slots
 constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
 constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
+constexpr int RG_SAMPLE_SLICES_MAX = 32;  // vocabulary slices per sampled row
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -81,6 +83,7 @@ struct rg_policy {
   float* att_ml = nullptr;
   int64_t att_rowchunks = 0;
   float* logits = nullptr;
+  float* sample_part = nullptr;   // [rows][RG_SAMPLE_SLICES_MAX][4]
   int32_t *page_tab = nullptr, *seq_grp = nullptr, *seq_npages = nullptr, *seq_nshared = nullptr,
           *seq_forced = nullptr, *grp_off = nullptr, *prompt_off = nullptr, *plen = nullptr, *G_dev = nullptr,
           *act_seq = nullptr, *act_tok = nullptr, *done = nullptr, *row_tab = nullptr, *row_pos = nullptr,
@@ -108,6 +111,9 @@ struct rg_policy {
 
   int32_t last_steps = 0;
 
+  hipStream_t cap_st = nullptr;   // private stream used only to capture decode-step graphs
+  bool use_graphs = true;
+
   int alloc(void** p, size_t bytes) {
     bytes = std::max<size_t>(bytes, 256);
     hipError_t e = hipMalloc(p, bytes);
@@ -123,6 +129,7 @@ struct rg_policy {
     if (h_ring) (void)hipHostFree(h_ring);
     for (auto& e : ring_ev) if (e) (void)hipEventDestroy(e);
     for (auto& e : prof_ev) if (e) (void)hipEventDestroy(e);
+    if (cap_st) (void)hipStreamDestroy(cap_st);
   }
 };
 
@@ -201,9 +208,10 @@ void plan(const rg_policy* pol, int N, int rows_ub, int K, int* S, int* kps) {
 
 // One projection with its epilogue; the split plan and workspace are filled in here.
 int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const void* W, int N, const int* d_rows,
-         int rows_ub, GemmEpi ep, bool allow_split = true) {
+         int rows_ub, GemmEpi ep, bool allow_split = true, int* splits_out = nullptr) {
   int S = 1, kps = K;
   if (allow_split) plan(pol, N, rows_ub, K, &S, &kps);
+  if (splits_out) *splits_out = S;
   ep.part = pol->cpart;
   ep.part_stride = (int64_t)rows_ub * N;
   const bool needs_part = S > 1 || pol->dtype != RG_DTYPE_BF16;
@@ -220,12 +228,12 @@ int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const v
 int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max, bool final_norm_rows) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
+  // chunks per row: enough work items to cover the chip, at least ~256 tokens
+  // each for the longest context, at most 16384 tokens each
   int n_chunks = 1;
   if ((int64_t)rows_ub * pol->nkv < RG_ATT_TARGET)
     n_chunks = (int)std::min<int64_t>(ceil_div(RG_ATT_TARGET, (int64_t)rows_ub * pol->nkv), ceil_div(ctx_max, 256));
-  n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16384)});
-  const int chunk_len = (int)ceil_div(ceil_div(ctx_max, n_chunks), 64) * 64;
-  n_chunks = (int)ceil_div(ctx_max, chunk_len);
+  n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16000)});
   if ((int64_t)rows_ub * n_chunks > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
   const float eps = pol->cfg.rms_eps;
   GemmEpi qkv{};
@@ -235,6 +243,7 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
   qkv.rope_cos = pol->rope_cos; qkv.rope_sin = pol->rope_sin; qkv.n_q = pol->nq; qkv.n_kv = pol->nkv; qkv.hd = pol->hd;
   GemmEpi resid{};
   resid.mode = GEMM_EPI_RESIDUAL; resid.x = pol->x; resid.ldx = pol->d;
+  resid.norm_eps = eps; resid.norm_out = ActOut{pol->abuf, pol->a_plane};
   GemmEpi swig{};
   swig.mode = GEMM_EPI_SWIGLU; swig.act = ActOut{pol->abuf2, pol->a_plane}; swig.act_ld = pol->F;
   int rc;
@@ -244,20 +253,27 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     if ((rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, d_rows, rows_ub, qkv)))
       return rc;
     LAUNCH(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
-                                       pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, chunk_len, n_chunks,
+                                       pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, ctx_max, n_chunks,
                                        pol->att_o, pol->att_ml, d_rows, rows_ub, st));
     LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
-                                              chunk_len, n_chunks, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
-    if ((rc = gemm(pol, st, RG_K_GEMM_O, pol->abuf2, pol->q_dim, pol->w_o[l], pol->d, d_rows, rows_ub, resid)))
+                                              n_chunks, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+    // O projection + residual, then the MLP norm into abuf (fused into the
+    // split epilogue when K is split)
+    int S;
+    resid.norm_g = pol->g_ffn[l];
+    if ((rc = gemm(pol, st, RG_K_GEMM_O, pol->abuf2, pol->q_dim, pol->w_o[l], pol->d, d_rows, rows_ub, resid, true, &S)))
       return rc;
-    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_ffn[l], pol->d, eps, pol->abuf, pol->a_plane,
-                                         nullptr, d_rows, rows_ub, st));
+    if (S == 1 || pol->dtype != RG_DTYPE_BF16)
+      LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_ffn[l], pol->d, eps, pol->abuf, pol->a_plane,
+                                           nullptr, d_rows, rows_ub, st));
     if ((rc = gemm(pol, st, RG_K_GEMM_GU, pol->abuf, pol->d, pol->w_gu[l], 2 * pol->F, d_rows, rows_ub, swig)))
       return rc;
-    if ((rc = gemm(pol, st, RG_K_GEMM_DOWN, pol->abuf2, pol->F, pol->w_down[l], pol->d, d_rows, rows_ub, resid)))
-      return rc;
     const float* gnext = l + 1 < pol->L ? pol->g_attn[l + 1] : (final_norm_rows ? pol->w_final : nullptr);
-    if (gnext)
+    resid.norm_g = gnext;
+    if ((rc = gemm(pol, st, RG_K_GEMM_DOWN, pol->abuf2, pol->F, pol->w_down[l], pol->d, d_rows, rows_ub, resid, true,
+                   &S)))
+      return rc;
+    if (gnext && (S == 1 || pol->dtype != RG_DTYPE_BF16))
       LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, gnext, pol->d, eps, pol->abuf, pol->a_plane, nullptr,
                                            d_rows, rows_ub, st));
   }
@@ -273,6 +289,69 @@ int run_head(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, con
   GemmEpi store{};
   store.mode = GEMM_EPI_STORE; store.C = pol->logits; store.ldc = pol->V;
   return gemm(pol, st, RG_K_GEMM_LM, pol->abuf, pol->d, pol->w_lm, pol->V, d_rows, rows_ub, store, false);
+}
+
+// Row bound used for a decode step: the host's bound rounded up, so that the
+// few distinct bounds share split plans and captured graphs.
+int row_bucket(int m) {
+  if (m <= 16) return 16;
+  if (m <= 32) return 32;
+  if (m <= 64) return 64;
+  if (m <= 128) return 128;
+  if (m <= 256) return 256;
+  if (m <= 384) return 384;
+  return (int)ceil_div(m, 256) * 256;
+}
+
+// Vocabulary slices per sampled row: about 1024 blocks in all.
+int sample_slices(int rows_ub) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(RG_SAMPLE_SLICES_MAX, ceil_div(1024, std::max(1, rows_ub))));
+}
+
+// Every kernel of one decode step (t >= 1, read on the device from state[8]).
+int enqueue_step(rg_policy* pol, hipStream_t st, int rows_ub, int ctx_max, SampleArgs sm, const CompactArgs& ca) {
+  sm.n_slices = sample_slices(rows_ub);
+  int rc;
+  LAUNCH(RG_K_EMBED, launch_decode_rows(pol->dtype, pol->w_embed, pol->d, pol->act_seq, pol->act_tok, pol->seq_grp,
+                                        pol->plen, pol->state + 8, pol->row_tab, pol->row_pos, pol->x, pol->state,
+                                        rows_ub, st));
+  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                       pol->a_plane, nullptr, pol->state, rows_ub, st));
+  if ((rc = run_layers(pol, st, pol->state, rows_ub, ctx_max, true))) return rc;
+  if ((rc = run_head(pol, st, pol->state, rows_ub, nullptr))) return rc;
+  LAUNCH(RG_K_SAMPLE, launch_sample(sm, rows_ub, st));
+  LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
+  return RG_OK;
+}
+
+// A decode-step graph per row bucket, captured on first use in a rollout.
+struct StepGraphs {
+  std::vector<std::pair<int, hipGraphExec_t>> execs;
+  ~StepGraphs() {
+    for (auto& g : execs) (void)hipGraphExecDestroy(g.second);
+  }
+};
+
+int step_graph(rg_policy* pol, StepGraphs& gs, int rows_ub, int ctx_max, const SampleArgs& sm,
+               const CompactArgs& ca, hipGraphExec_t* out) {
+  for (auto& g : gs.execs)
+    if (g.first == rows_ub) { *out = g.second; return RG_OK; }
+  HIPTRY(hipStreamBeginCapture(pol->cap_st, hipStreamCaptureModeThreadLocal));
+  const int rc = enqueue_step(pol, pol->cap_st, rows_ub, ctx_max, sm, ca);
+  hipGraph_t graph = nullptr;
+  const hipError_t e = hipStreamEndCapture(pol->cap_st, &graph);
+  if (rc) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return rc;
+  }
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (ei != hipSuccess) return fail(RG_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(ei));
+  gs.execs.emplace_back(rows_ub, exec);
+  *out = exec;
+  return RG_OK;
 }
 
 int copy_weight(rg_policy* pol, void* dst, const void* src, size_t bytes, const char* what) {
@@ -429,6 +508,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       {(void**)&pol->att_o, (size_t)(pol->att_rowchunks * pol->nq * pol->hd * 4)},
       {(void**)&pol->att_ml, (size_t)(pol->att_rowchunks * pol->nq * 2 * 4)},
       {(void**)&pol->logits, (size_t)(std::max(S, P) * pol->V * 4)},
+      {(void**)&pol->sample_part, (size_t)(std::max(S, P) * RG_SAMPLE_SLICES_MAX * 4 * 4)},
       {(void**)&pol->page_tab, (size_t)((S + P) * pol->max_pages * 4)},
       {(void**)&pol->seq_grp, (size_t)(S * 4)},
       {(void**)&pol->seq_npages, (size_t)(S * 4)},
@@ -468,6 +548,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
       if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipEventCreate: ") + hipGetErrorString(e)));
     }
+    e = hipStreamCreateWithFlags(&pol->cap_st, hipStreamNonBlocking);
+    if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipStreamCreate: ") + hipGetErrorString(e)));
+    const char* env = getenv("RG_NO_GRAPHS");
+    pol->use_graphs = !(env && env[0] == '1');
   }
   *out = pol;
   return RG_OK;
@@ -588,6 +672,7 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   sm.logprobs_out = logprobs; sm.next_tok = pol->act_tok; sm.done = pol->done; sm.d_rows = pol->state;
   sm.bad_token = pol->state + 7;
   sm.logits = pol->logits;
+  sm.d_t = pol->state + 8;
   CompactArgs ca{};
   ca.max_new = max_new; ca.page_tok = pol->page_tok; ca.max_pages = pol->max_pages; ca.n_seq = Ni;
   ca.act_seq = pol->act_seq; ca.act_tok = pol->act_tok; ca.done = pol->done; ca.seq_grp = pol->seq_grp;
@@ -597,16 +682,17 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
 
   auto snapshot = [&](int t) -> int {
     const int slot = t % RG_RING;
-    HIPTRY(hipMemcpyAsync(pol->h_ring + 8 * slot, pol->state, 32, hipMemcpyDeviceToHost, st));
+    HIPTRY(hipMemcpyAsync(pol->h_ring + 8 * slot, pol->state, 8 * sizeof(int32_t), hipMemcpyDeviceToHost, st));
     HIPTRY(hipEventRecord(pol->ring_ev[slot], st));
     return RG_OK;
   };
 
-  // step 0
+  // step 0: every sibling samples from its prompt's logits
   pol->prof_phase = 1;
-  sm.t = 0; sm.logits_by_group = 1;
+  sm.logits_by_group = 1;
+  sm.part = pol->sample_part;
+  sm.n_slices = sample_slices(Ni);
   LAUNCH(RG_K_SAMPLE, launch_sample(sm, Ni, st));
-  ca.t = 0;
   LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
   if ((rc = snapshot(0))) return rc;
   HIPTRY(hipEventSynchronize(pol->ring_ev[0]));
@@ -615,7 +701,14 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   bool oom = pol->h_ring[2] != 0;
   int n_steps = m_ub == 0 ? 1 : 0;
 
+  // steps t >= 1, as captured graphs (one per row bucket) or, when kernels
+  // are being timed, as direct launches; both run the same kernels with the
+  // same arguments.  The attention chunk plan covers the longest possible
+  // context, so it does not change from step to step.
   sm.logits_by_group = 0;
+  const int ctx_all = max_plen + max_new;
+  StepGraphs graphs;
+  const bool graphs_on = pol->use_graphs && !pol->prof;
   for (int t = 1; t < max_new && n_steps == 0 && !oom; ++t) {
     // refresh the upper bound from completed snapshots; never run too far ahead
     while (known_t + 1 < t) {
@@ -628,16 +721,14 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
       if (m_ub == 0) { n_steps = known_t + 1; break; }
     }
     if (n_steps || oom) break;
-    LAUNCH(RG_K_EMBED, launch_decode_rows(pol->dtype, pol->w_embed, pol->d, pol->act_seq, pol->act_tok, pol->seq_grp,
-                                          pol->plen, t, pol->row_tab, pol->row_pos, pol->x, pol->state, m_ub, st));
-    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
-                                         pol->a_plane, nullptr, pol->state, m_ub, st));
-    if ((rc = run_layers(pol, st, pol->state, m_ub, max_plen + t, true))) return rc;
-    if ((rc = run_head(pol, st, pol->state, m_ub, nullptr))) return rc;
-    sm.t = t;
-    LAUNCH(RG_K_SAMPLE, launch_sample(sm, m_ub, st));
-    ca.t = t;
-    LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
+    const int rows_ub = std::min(row_bucket(m_ub), pol->m_act);
+    if (graphs_on) {
+      hipGraphExec_t exec;
+      if ((rc = step_graph(pol, graphs, rows_ub, ctx_all, sm, ca, &exec))) return rc;
+      HIPTRY(hipGraphLaunch(exec, st));
+    } else {
+      if ((rc = enqueue_step(pol, st, rows_ub, ctx_all, sm, ca))) return rc;
+    }
     if ((rc = snapshot(t))) return rc;
     last_t = t;
   }

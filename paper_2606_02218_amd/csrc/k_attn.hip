@@ -16,10 +16,19 @@
 // page ids are read once into LDS and the next block's K and V are loaded
 // while the current block is multiplied.
 // fp32 KV (fp32 models): a plain per-token VALU kernel.
+#include <algorithm>
+
 #include "rg_device.h"
 #include "rg_kernels.h"
 
 namespace {
+
+// Context chunk of a row: its context is cut into at most n_chunks chunks of
+// equal length, rounded up to 32 tokens (so chunks start on 32-token blocks)
+// and at least 128 tokens; the attention kernel and the merge both use this.
+__device__ __forceinline__ int att_chunk_len(int ctx, int n_chunks) {
+  return max(128, ((ctx + n_chunks - 1) / n_chunks + 31) & ~31);
+}
 
 constexpr int ATT_TILE = 256;   // tokens scored per tile (one per thread)
 constexpr int ATT_MAX_REP = 8;  // query heads per kv head
@@ -46,16 +55,17 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
                                                    const KV* __restrict__ pool, KvGeom g, int layer,
                                                    const int32_t* __restrict__ page_tab, int tab_stride,
                                                    const int32_t* __restrict__ row_tab,
-                                                   const int32_t* __restrict__ row_pos, int chunk_len,
+                                                   const int32_t* __restrict__ row_pos,
                                                    int n_chunks, float* __restrict__ part_o,
                                                    float* __restrict__ part_ml, const int* __restrict__ d_rows) {
   const int r = blockIdx.z;
   if (r >= *d_rows) return;
   const int kvh = blockIdx.y, chunk = blockIdx.x;
   const int ctx = row_pos[r] + 1;
-  const int c0 = chunk * chunk_len;
+  const int clen = att_chunk_len(ctx, n_chunks);
+  const int c0 = chunk * clen;
   if (c0 >= ctx) return;
-  const int c1 = min(ctx, c0 + chunk_len);
+  const int c1 = min(ctx, c0 + clen);
   const int rep = n_q / n_kv;
   const int tid = threadIdx.x;
   const float scale = 1.0f / sqrtf((float)hd);
@@ -164,6 +174,7 @@ __device__ __forceinline__ void split8(const float* v, bf16x8_t& hi, bf16x8_t& l
 }
 
 constexpr int ATT_MAX_CHUNK_PAGES = 1024;   // a chunk spans at most 16384 tokens
+constexpr int ATT_MAX_MERGE = 1024;         // chunks per row
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -202,7 +213,7 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
                                                        const bf16_t* __restrict__ pool, KvGeom g, int layer,
                                                        const int32_t* __restrict__ page_tab, int tab_stride,
                                                        const int32_t* __restrict__ row_tab,
-                                                       const int32_t* __restrict__ row_pos, int chunk_len,
+                                                       const int32_t* __restrict__ row_pos,
                                                        int n_chunks, int rows_ub, float* __restrict__ part_o,
                                                        float* __restrict__ part_ml, const int* __restrict__ d_rows) {
   static_assert(HD % 32 == 0 && HD <= 256, "head_dim");
@@ -220,9 +231,10 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
   const int r = (int)(w / ((int64_t)n_chunks * n_kv));
   if (r >= *d_rows) return;
   const int ctx = row_pos[r] + 1;
-  const int c0 = chunk * chunk_len;
+  const int clen = att_chunk_len(ctx, n_chunks);
+  const int c0 = chunk * clen;
   if (c0 >= ctx) return;
-  const int c1 = min(ctx, c0 + chunk_len);
+  const int c1 = min(ctx, c0 + clen);
   const int rep = n_q / n_kv;
   const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
 
@@ -337,27 +349,40 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
 
 template <int SPLIT>
 __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __restrict__ part_ml, int n_q, int hd,
-                             const int32_t* __restrict__ row_pos, int chunk_len, int n_chunks, ActOut out,
+                             const int32_t* __restrict__ row_pos, int n_chunks, ActOut out,
                              const int* __restrict__ d_rows) {
   const int r = blockIdx.x;
   if (r >= *d_rows) return;
   const int h = blockIdx.y;
-  const int nc = (row_pos[r] + chunk_len) / chunk_len;   // chunks holding context
-  float M = -INFINITY;
-  for (int c = 0; c < nc; ++c) M = fmaxf(M, part_ml[(((int64_t)r * n_chunks + c) * n_q + h) * 2]);
-  float L = 0.f;
-  for (int c = 0; c < nc; ++c) {
-    const float* ml = part_ml + (((int64_t)r * n_chunks + c) * n_q + h) * 2;
-    L += expf(ml[0] - M) * ml[1];
+  const int ctx = row_pos[r] + 1;
+  const int clen = att_chunk_len(ctx, n_chunks);
+  const int nc = (ctx + clen - 1) / clen;   // chunks holding context
+  __shared__ float sw[ATT_MAX_MERGE];       // chunk weights exp(m_c - M) / L
+  // (max, sum) of every chunk: one thread per chunk, then a wave reduction
+  const int64_t rb = (int64_t)r * n_chunks;
+  float m = -INFINITY;
+  for (int c = threadIdx.x; c < nc; c += blockDim.x) m = fmaxf(m, part_ml[((rb + c) * n_q + h) * 2]);
+  __shared__ float red[16];
+  const float M = block_max(m, red);
+  float l = 0.f;
+  for (int c = threadIdx.x; c < nc; c += blockDim.x) {
+    const float* ml = part_ml + ((rb + c) * n_q + h) * 2;
+    const float w = expf(ml[0] - M);
+    sw[c] = w;
+    l += w * ml[1];
   }
-  const float invL = 1.0f / L;
+  const float invL = 1.0f / block_sum(l, red);
   for (int d = threadIdx.x; d < hd; d += blockDim.x) {
-    float o = 0.f;
-    for (int c = 0; c < nc; ++c) {
-      const int64_t b = ((int64_t)r * n_chunks + c) * n_q + h;
-      o += expf(part_ml[b * 2] - M) * part_o[b * hd + d];
+    float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;   // independent sums keep several loads in flight
+    int c = 0;
+    for (; c + 4 <= nc; c += 4) {
+      o0 += sw[c] * part_o[((rb + c) * n_q + h) * hd + d];
+      o1 += sw[c + 1] * part_o[((rb + c + 1) * n_q + h) * hd + d];
+      o2 += sw[c + 2] * part_o[((rb + c + 2) * n_q + h) * hd + d];
+      o3 += sw[c + 3] * part_o[((rb + c + 3) * n_q + h) * hd + d];
     }
-    act_store<SPLIT>(out, ((int64_t)r * n_q + h) * hd + d, o * invL);
+    for (; c < nc; ++c) o0 += sw[c] * part_o[((rb + c) * n_q + h) * hd + d];
+    act_store<SPLIT>(out, ((int64_t)r * n_q + h) * hd + d, ((o0 + o1) + (o2 + o3)) * invL);
   }
 }
 
@@ -365,18 +390,21 @@ __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __re
 
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool,
                             KvGeom g, int layer, const int32_t* page_tab, int tab_stride,
-                            const int32_t* row_tab, const int32_t* row_pos, int chunk_len, int n_chunks,
+                            const int32_t* row_tab, const int32_t* row_pos, int max_ctx, int n_chunks,
                             float* part_o, float* part_ml, const int* d_rows, int rows_ub, hipStream_t st) {
+  if (n_chunks < 1 || n_chunks > ATT_MAX_MERGE ||
+      std::max(128, (max_ctx + n_chunks - 1) / n_chunks + 31) > 16 * ATT_MAX_CHUNK_PAGES)
+    return hipErrorInvalidValue;
   if (rows_ub <= 0) return hipSuccess;
   dim3 grid(n_chunks, n_kv, rows_ub);
   if (dtype == 1) {
-    // two 16-slot pages per 32-token block, blocks 32-aligned inside a chunk
-    if (g.page_tok != 16 || chunk_len % 32 != 0 || chunk_len > 16 * ATT_MAX_CHUNK_PAGES) return hipErrorInvalidValue;
+    // two 16-slot pages per 32-token block
+    if (g.page_tok != 16) return hipErrorInvalidValue;
     const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
     hipLaunchKernelGGL(k_attention_mfma<HD>, grid1, dim3(64), 0, st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
-                       page_tab, tab_stride, row_tab, row_pos, chunk_len, n_chunks, rows_ub, part_o, part_ml, d_rows)
+                       page_tab, tab_stride, row_tab, row_pos, n_chunks, rows_ub, part_o, part_ml, d_rows)
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;
@@ -385,23 +413,23 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
 #undef RG_ATT_MFMA
   } else
     hipLaunchKernelGGL(k_attention<float>, grid, dim3(256), 0, st, q, n_q, n_kv, head_dim, (const float*)kv_pool,
-                       g, layer, page_tab, tab_stride, row_tab, row_pos, chunk_len, n_chunks, part_o, part_ml,
-                       d_rows);
+                       g, layer, page_tab, tab_stride, row_tab, row_pos, n_chunks, part_o, part_ml, d_rows);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_ml, int n_q, int head_dim,
-                             const int32_t* row_pos, int chunk_len, int n_chunks, void* out, int64_t a_plane,
+                             const int32_t* row_pos, int n_chunks, void* out, int64_t a_plane,
                              const int* d_rows, int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
+  if (n_chunks < 1 || n_chunks > ATT_MAX_MERGE) return hipErrorInvalidValue;
   dim3 grid(rows_ub, n_q);
   int threads = head_dim >= 64 ? 64 * ((head_dim + 63) / 64) : 64;
   const ActOut o{out, a_plane};
   if (dtype == 1)
     hipLaunchKernelGGL(k_attn_merge<1>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos,
-                       chunk_len, n_chunks, o, d_rows);
+                       n_chunks, o, d_rows);
   else
     hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos,
-                       chunk_len, n_chunks, o, d_rows);
+                       n_chunks, o, d_rows);
   return hipGetLastError();
 }

@@ -46,11 +46,18 @@ __device__ __forceinline__ void kv_store(KV* p, float v);
 template <> __device__ __forceinline__ void kv_store<float>(float* p, float v) { *p = v; }
 template <> __device__ __forceinline__ void kv_store<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
 
-// Sum of the split partials of element (r, c), in split order.
+// Sum of the split partials of element (r, c), in split order.  All loads
+// (at most GEMM_MAX_SPLITS) are issued before the first add.
 __device__ __forceinline__ float split_sum(const GemmEpi& ep, int S, int64_t off) {
-  float v = 0.f;
-  for (int s = 0; s < S; ++s) v += ep.part[s * ep.part_stride + off];
-  return v;
+  const float* p = ep.part + off;
+  const int64_t st = ep.part_stride;
+  float v[GEMM_MAX_SPLITS];
+#pragma unroll
+  for (int s = 0; s < GEMM_MAX_SPLITS; ++s) v[s] = s < S ? p[s * st] : 0.f;
+  float acc = 0.f;
+#pragma unroll
+  for (int s = 0; s < GEMM_MAX_SPLITS; ++s) acc += v[s];
+  return acc;
 }
 
 // QKV epilogue of row r for packed column c (a lower-half tile column: bit 4
@@ -257,6 +264,26 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   }
 }
 
+// Residual add of the split partials followed by the next RMSNorm of the row
+// (x += sum; act = x / sqrt(mean(x^2) + eps) * g): one 256-thread block per row.
+template <int SPLIT>
+__global__ __launch_bounds__(512) void k_split_residual_norm(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+  const int r = blockIdx.x;
+  if (r >= *d_rows) return;
+  __shared__ float red[16];
+  float* xr = ep.x + (int64_t)r * ep.ldx;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < N; c += blockDim.x) {
+    const float v = xr[c] + split_sum(ep, S, (int64_t)r * N + c);
+    xr[c] = v;
+    ss = fmaf(v, v, ss);
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)N + ep.norm_eps);
+  for (int c = threadIdx.x; c < N; c += blockDim.x)
+    act_store<SPLIT>(ep.norm_out, (int64_t)r * N + c, xr[c] * inv * ep.norm_g[c]);
+}
+
 // Sum of split partials + epilogue: one block of 128 threads per (128
 // columns, row).  SPLIT: activation output as hi/lo bf16 planes.
 template <int EPI, int SPLIT, typename KV>
@@ -308,6 +335,10 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
 
 template <int SPLIT, typename KV>
 hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, const GemmEpi& ep, hipStream_t st) {
+  if (ep.mode == GEMM_EPI_RESIDUAL && ep.norm_g) {
+    hipLaunchKernelGGL((k_split_residual_norm<SPLIT>), dim3(rows_ub), dim3(512), 0, st, d_rows, N, S, ep);
+    return hipGetLastError();
+  }
   dim3 grid((N + 127) / 128, rows_ub);
   switch (ep.mode) {
     case GEMM_EPI_STORE: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_STORE, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
@@ -336,6 +367,7 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
                        int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
   if ((splits > 1 || dtype != 1) && !ep.part) return hipErrorInvalidValue;
+  if (splits > GEMM_MAX_SPLITS) return hipErrorInvalidValue;
   if ((ep.mode == GEMM_EPI_SWIGLU || ep.mode == GEMM_EPI_QKV) && N % 32) return hipErrorInvalidValue;
   if (ep.mode == GEMM_EPI_QKV && (ep.hd % 32 || 128 % ep.hd)) return hipErrorInvalidValue;
   hipError_t e;

@@ -22,14 +22,15 @@ __global__ void k_embed(const T* __restrict__ embed, int d, int V, const int32_t
 template <typename T>
 __global__ void k_decode_rows(const T* __restrict__ embed, int d, const int32_t* __restrict__ act_seq,
                               const int32_t* __restrict__ act_tok, const int32_t* __restrict__ seq_grp,
-                              const int32_t* __restrict__ plen, int t, int32_t* __restrict__ row_tab,
+                              const int32_t* __restrict__ plen, const int* __restrict__ d_t,
+                              int32_t* __restrict__ row_tab,
                               int32_t* __restrict__ row_pos, float* __restrict__ x, const int* __restrict__ d_rows) {
   const int r = blockIdx.x;
   if (r >= *d_rows) return;
   const int s = act_seq[r];
   if (threadIdx.x == 0) {
     row_tab[r] = s;
-    row_pos[r] = plen[seq_grp[s]] + t - 1;
+    row_pos[r] = plen[seq_grp[s]] + *d_t - 1;
   }
   const T* e = embed + (int64_t)act_tok[r] * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ld_f32<T>(e + i);
@@ -131,15 +132,16 @@ hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_
 }
 
 hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq, const int32_t* act_tok,
-                              const int32_t* seq_grp, const int32_t* plen, int t, int32_t* row_tab, int32_t* row_pos,
+                              const int32_t* seq_grp, const int32_t* plen, const int* d_t, int32_t* row_tab,
+                              int32_t* row_pos,
                               float* x, const int* d_rows, int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
   if (dtype == 1)
     hipLaunchKernelGGL(k_decode_rows<bf16_t>, dim3(rows_ub), dim3(256), 0, st, (const bf16_t*)embed, d, act_seq, act_tok,
-                       seq_grp, plen, t, row_tab, row_pos, x, d_rows);
+                       seq_grp, plen, d_t, row_tab, row_pos, x, d_rows);
   else
     hipLaunchKernelGGL(k_decode_rows<float>, dim3(rows_ub), dim3(256), 0, st, (const float*)embed, d, act_seq, act_tok,
-                       seq_grp, plen, t, row_tab, row_pos, x, d_rows);
+                       seq_grp, plen, d_t, row_tab, row_pos, x, d_rows);
   return hipGetLastError();
 }
 

@@ -31,26 +31,34 @@ __device__ int block_excl_scan(int v, int* lds, int* total) {
 }
 
 // ------------------------------------------------------------------ sampling
+// Two kernels.  k_sample_slice: block (slice, row) scans one slice of the
+// row's vocabulary -- Gumbel scores, running logsumexp of z/T -- and writes
+// the slice's (best score, best id, max, sum).  k_sample_pick: one block per
+// row combines the slices in order (ties to the lowest id), decides the
+// token and writes the outputs.
 constexpr int SAMPLE_THREADS = 256;
 
-__global__ __launch_bounds__(SAMPLE_THREADS) void k_sample(SampleArgs a) {
-  const int r = blockIdx.x;
+__global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
+  const int r = blockIdx.y;
   if (r >= *a.d_rows) return;
   const int tid = threadIdx.x;
+  const int t = *a.d_t;
   const int s = a.act_seq[r];
   const int lrow = a.logits_by_group ? a.seq_grp[s] : r;
   const float* z = a.logits + (int64_t)lrow * a.V;
   const int L = a.forced_len ? a.forced_len[s] : -1;
-  const bool mask_eos = L > 0 && a.t < L - 1;
+  const bool mask_eos = L > 0 && t < L - 1;
   const float T = a.temperature;
+  const int nb = a.V >> 3;                                  // 8-token Philox blocks
+  const int per = (nb + a.n_slices - 1) / a.n_slices;
+  const int vb0 = blockIdx.x * per, vb1 = min(nb, vb0 + per);
 
   float best = -INFINITY;
   int best_v = 0x7FFFFFFF;
   float m = -INFINITY, sum = 0.f;
-  const int nb = a.V >> 3;
-  for (int vb = tid; vb < nb; vb += SAMPLE_THREADS) {
+  for (int vb = vb0 + tid; vb < vb1; vb += SAMPLE_THREADS) {
     rg_u64x4 c;
-    c.v[0] = (uint64_t)vb; c.v[1] = (uint64_t)a.t; c.v[2] = (uint64_t)s; c.v[3] = 0;
+    c.v[0] = (uint64_t)vb; c.v[1] = (uint64_t)t; c.v[2] = (uint64_t)s; c.v[3] = 0;
     rg_u64x4 w = rg_philox4x64_10(c, a.seed, RG_TAG_GUMBEL);
     const float4 z0 = *reinterpret_cast<const float4*>(z + vb * 8);
     const float4 z1 = *reinterpret_cast<const float4*>(z + vb * 8 + 4);
@@ -67,8 +75,12 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample(SampleArgs a) {
       if (mask_eos && v == a.eos) sc = -INFINITY;
       if (sc > best || (sc == best && v < best_v)) { best = sc; best_v = v; }
     }
+    if (a.dump_logits && t < a.dump_steps) {
+      float* dst = a.dump_logits + ((int64_t)t * a.n_seq + s) * a.V + vb * 8;
+      *reinterpret_cast<float4*>(dst) = z0;
+      *reinterpret_cast<float4*>(dst + 4) = z1;
+    }
   }
-  // block reductions: argmax (score, lowest id) and logsumexp
   __shared__ float sb[SAMPLE_THREADS], sm[SAMPLE_THREADS], ss[SAMPLE_THREADS];
   __shared__ int sv[SAMPLE_THREADS];
   sb[tid] = best; sv[tid] = best_v; sm[tid] = m; ss[tid] = sum;
@@ -79,28 +91,48 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample(SampleArgs a) {
       if (b2 > sb[tid] || (b2 == sb[tid] && v2 < sv[tid])) { sb[tid] = b2; sv[tid] = v2; }
       const float m1 = sm[tid], m2 = sm[tid + o];
       const float mm = fmaxf(m1, m2);
-      float s1 = ss[tid], s2 = ss[tid + o];
-      ss[tid] = (m1 == -INFINITY ? 0.f : s1 * expf(m1 - mm)) + (m2 == -INFINITY ? 0.f : s2 * expf(m2 - mm));
+      ss[tid] = (m1 == -INFINITY ? 0.f : ss[tid] * expf(m1 - mm)) + (m2 == -INFINITY ? 0.f : ss[tid + o] * expf(m2 - mm));
       sm[tid] = mm;
     }
     __syncthreads();
   }
   if (tid == 0) {
-    int y = sv[0];
-    if (L > 0 && a.t == L - 1) y = a.eos;
-    int fed = a.force_tokens ? a.force_tokens[(int64_t)s * a.max_new + a.t] : y;
-    if (fed < 0 || fed >= a.V) { fed = a.eos; a.bad_token[0] = 1; }   // invalid forced id: stop this sequence
-    const float lse = sm[0] + logf(ss[0]);
-    const float lp = z[fed] / T - lse;
-    a.tokens_out[(int64_t)s * a.max_new + a.t] = y;
-    a.logprobs_out[(int64_t)s * a.max_new + a.t] = lp;
-    a.next_tok[r] = fed;
-    a.done[r] = (fed == a.eos || a.t + 1 == a.max_new) ? 1 : 0;
+    float* p = a.part + ((int64_t)r * a.n_slices + blockIdx.x) * 4;
+    p[0] = sb[0];
+    p[1] = __int_as_float(sv[0]);
+    p[2] = sm[0];
+    p[3] = ss[0];
   }
-  if (a.dump_logits && a.t < a.dump_steps) {
-    float* dst = a.dump_logits + ((int64_t)a.t * a.n_seq + s) * a.V;
-    for (int v = tid; v < a.V; v += SAMPLE_THREADS) dst[v] = z[v];
+}
+
+__global__ __launch_bounds__(64) void k_sample_pick(SampleArgs a) {
+  const int r = blockIdx.x;
+  if (r >= *a.d_rows || threadIdx.x != 0) return;
+  const int t = *a.d_t;
+  const int s = a.act_seq[r];
+  const int lrow = a.logits_by_group ? a.seq_grp[s] : r;
+  const float* z = a.logits + (int64_t)lrow * a.V;
+  const int L = a.forced_len ? a.forced_len[s] : -1;
+  float best = -INFINITY, m = -INFINITY, sum = 0.f;
+  int y = 0x7FFFFFFF;
+  for (int k = 0; k < a.n_slices; ++k) {
+    const float* p = a.part + ((int64_t)r * a.n_slices + k) * 4;
+    const float b2 = p[0];
+    const int v2 = __float_as_int(p[1]);
+    if (b2 > best || (b2 == best && v2 < y)) { best = b2; y = v2; }
+    const float mm = fmaxf(m, p[2]);
+    sum = (m == -INFINITY ? 0.f : sum * expf(m - mm)) + (p[2] == -INFINITY ? 0.f : p[3] * expf(p[2] - mm));
+    m = mm;
   }
+  if (L > 0 && t == L - 1) y = a.eos;
+  int fed = a.force_tokens ? a.force_tokens[(int64_t)s * a.max_new + t] : y;
+  if (fed < 0 || fed >= a.V) { fed = a.eos; a.bad_token[0] = 1; }   // invalid forced id: stop this sequence
+  const float lse = m + logf(sum);
+  const float lp = z[fed] / a.temperature - lse;
+  a.tokens_out[(int64_t)s * a.max_new + t] = y;
+  a.logprobs_out[(int64_t)s * a.max_new + t] = lp;
+  a.next_tok[r] = fed;
+  a.done[r] = (fed == a.eos || t + 1 == a.max_new) ? 1 : 0;
 }
 
 // ------------------------------------------------------------------ retirement
@@ -113,6 +145,7 @@ __global__ __launch_bounds__(1024) void k_compact(CompactArgs a) {
   __shared__ int s_groups;
   const int tid = threadIdx.x;
   const int M = a.state[0];
+  const int t = a.state[8];
   int top = a.state[1];
   if (tid == 0) { s_ctx = 0; s_groups = 0; }
   __syncthreads();
@@ -133,7 +166,7 @@ __global__ __launch_bounds__(1024) void k_compact(CompactArgs a) {
     int tot;
     const int off = block_excl_scan(f, lds, &tot) + carry;
     if (dn) {
-      a.lengths[s] = a.t + 1;
+      a.lengths[s] = t + 1;
       const int32_t* tab = a.page_tab + (int64_t)s * a.max_pages + a.seq_nshared[s];
       for (int i = 0; i < f; ++i) a.free_stack[top + off + i] = tab[i];
       a.seq_npages[s] = a.seq_nshared[s];
@@ -152,7 +185,7 @@ __global__ __launch_bounds__(1024) void k_compact(CompactArgs a) {
       s = a.act_seq[r];
       tok = a.act_tok[r];
       keep = a.done[r] == 0;
-      need = keep && ((a.plen[a.seq_grp[s]] + a.t) % a.page_tok == 0);
+      need = keep && ((a.plen[a.seq_grp[s]] + t) % a.page_tok == 0);
     }
     __syncthreads();   // every read of this tile precedes any in-place write
     int ktot, ntot;
@@ -172,13 +205,14 @@ __global__ __launch_bounds__(1024) void k_compact(CompactArgs a) {
   }
   if (ncarry > top) oom = true;
   if (tid == 0) {
-    if (a.t < a.hist_cap) {
-      a.hist_active[a.t] = M;
-      a.hist_groups[a.t] = s_groups;
-      a.hist_ctx[a.t] = (int64_t)s_ctx;
+    if (t < a.hist_cap) {
+      a.hist_active[t] = M;
+      a.hist_groups[t] = s_groups;
+      a.hist_ctx[t] = (int64_t)s_ctx;
     }
     if (oom) { a.state[2] = 1; a.state[0] = 0; }
     else { a.state[0] = kcarry; a.state[1] = top - ncarry; }
+    a.state[8] = t + 1;   // the next step
   }
 }
 
@@ -270,6 +304,7 @@ __global__ __launch_bounds__(1024) void k_setup_scan(SetupArgs a) {
     a.state[5] = oom ? 0 : c_tok;   // no prefill rows (so no page writes) without room
     a.state[6] = oom ? 0 : a.P;
     a.state[7] = 0;
+    a.state[8] = 0;
   }
 }
 
@@ -359,7 +394,11 @@ __global__ __launch_bounds__(1024) void k_group_advantage(const float* __restric
 
 hipError_t launch_sample(const SampleArgs& a, int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_sample, dim3(rows_ub), dim3(SAMPLE_THREADS), 0, st, a);
+  if (a.n_slices < 1 || a.V % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_sample_slice, dim3(a.n_slices, rows_ub), dim3(SAMPLE_THREADS), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_sample_pick, dim3(rows_ub), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

@@ -25,6 +25,9 @@ struct KvGeom {
 int gemm_tile_rows(int dtype, int rows_ub);
 int gemm_tile_cols(int dtype, int rows_ub);
 
+// Largest split-K factor of a projection.
+constexpr int GEMM_MAX_SPLITS = 32;
+
 // Epilogue of a projection (see k_gemm.hip).
 enum { GEMM_EPI_STORE = 0,      // C[r][n] = y
        GEMM_EPI_RESIDUAL = 1,   // x[r][n] += y
@@ -35,6 +38,8 @@ struct GemmEpi {
   int mode;
   float* C; int ldc;                      // STORE
   float* x; int ldx;                      // RESIDUAL
+  const float* norm_g; float norm_eps; ActOut norm_out;   // RESIDUAL with K split: then RMSNorm the row
+                                                          // into norm_out (ignored without a split)
   ActOut act; int act_ld;                 // SWIGLU
   float* q_out; void* kv_pool; KvGeom geom; int layer;      // QKV
   const int32_t* page_tab; int tab_stride; const int32_t* row_tab; const int32_t* row_pos;
@@ -53,11 +58,11 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
 hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_t* tok, float* x,
                         int32_t* bad_token, const int* d_rows, int rows_ub, hipStream_t st);
 
-// Decode row setup for step t >= 1: row r (< *d_rows) feeds act_tok[r] for
-// sequence s = act_seq[r] at position plen[grp[s]] + t - 1; writes row_tab,
-// row_pos and the embedded token into x.
+// Decode row setup for step t = *d_t >= 1: row r (< *d_rows) feeds act_tok[r]
+// for sequence s = act_seq[r] at position plen[grp[s]] + t - 1; writes
+// row_tab, row_pos and the embedded token into x.
 hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq,
-                              const int32_t* act_tok, const int32_t* seq_grp, const int32_t* plen, int t,
+                              const int32_t* act_tok, const int32_t* seq_grp, const int32_t* plen, const int* d_t,
                               int32_t* row_tab, int32_t* row_pos, float* x, const int* d_rows,
                               int rows_ub, hipStream_t st);
 
@@ -72,19 +77,20 @@ hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, floa
                           const int32_t* src_rows, const int* d_rows, int rows_ub, hipStream_t st);
 
 // Paged causal attention.  Row r's context is positions 0..row_pos[r] of page
-// table row_tab[r]; it is split into n_chunks chunks of chunk_len tokens
-// (a multiple of 256); each (row, kv head, chunk) block writes a partial
-// (max, sum, unnormalised output) per query head.
+// table row_tab[r] (at most max_ctx tokens); each row cuts its own context
+// into n_chunks equal chunks (rounded up to 32 tokens); each (row, kv head,
+// chunk) work item writes a partial (max, sum, unnormalised output) per query
+// head.
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim,
                             const void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
-                            int tab_stride, const int32_t* row_tab, const int32_t* row_pos, int chunk_len,
+                            int tab_stride, const int32_t* row_tab, const int32_t* row_pos, int max_ctx,
                             int n_chunks, float* part_o, float* part_ml, const int* d_rows,
                             int rows_ub, hipStream_t st);
 
 // Merge the chunk partials of each (row, q head) into the activation operand
 // out [rows][n_q*head_dim].
 hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_ml, int n_q,
-                             int head_dim, const int32_t* row_pos, int chunk_len, int n_chunks, void* out,
+                             int head_dim, const int32_t* row_pos, int n_chunks, void* out,
                              int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
 
 // x[r][n] += sum_s C[s][r][n] (C may be NULL: no add; one block per 256
@@ -97,7 +103,8 @@ hipError_t launch_residual_norm(int dtype, const float* C, int64_t split_stride,
 struct SampleArgs {
   const float* logits;      // [rows][V] or [P][V] when logits_by_group
   int logits_by_group;      // step 0: logits row = seq_grp[s]
-  int V, eos, t, max_new;
+  int V, eos, max_new;
+  const int* d_t;           // device step index
   uint64_t seed;
   float temperature;
   const int32_t* act_seq;   // row -> sequence
@@ -110,16 +117,19 @@ struct SampleArgs {
   int32_t* done;            // [rows]
   int32_t* bad_token;       // set to 1 when a forced token id is outside [0, V)
   const int* d_rows;
+  float* part;              // [rows][n_slices][4] slice partials
+  int n_slices;             // vocabulary slices per row
 };
 hipError_t launch_sample(const SampleArgs& a, int rows_ub, hipStream_t st);
 
+// Retire/compact after the step whose index is state[8]; advances state[8].
 struct CompactArgs {
-  int t, max_new, page_tok, max_pages, n_seq;
+  int max_new, page_tok, max_pages, n_seq;
   int32_t* act_seq; int32_t* act_tok; const int32_t* done;
   const int32_t* seq_grp; const int32_t* plen;
   int32_t* page_tab; int32_t* seq_npages; const int32_t* seq_nshared;
   int32_t* free_stack;
-  int32_t* state;     // [0] active rows, [1] free-stack top, [2] out-of-pages flag
+  int32_t* state;     // [0] active rows, [1] free-stack top, [2] out-of-pages flag, [8] step
   int32_t* lengths;
   int32_t* hist_active; int32_t* hist_groups; int64_t* hist_ctx; int hist_cap;
 };
@@ -148,7 +158,8 @@ struct SetupArgs {
   int32_t* tokens_out; float* logprobs_out;
   int32_t* last_rows;      // [P] row of each prompt's last token
   // state: [0] active rows, [1] free-stack top, [2] out-of-pages flag, [3] page
-  // copies pending, [4] prefix pages, [5] prompt tokens, [6] prompts, [7] invalid token id seen
+  // copies pending, [4] prefix pages, [5] prompt tokens, [6] prompts, [7] invalid token id seen,
+  // [8] step index
 };
 hipError_t launch_setup(const SetupArgs& a, hipStream_t st);
 

@@ -2,6 +2,7 @@
 
     python -m paper_2606_02218_amd.prof stats DIR              # per-kernel time table
     python -m paper_2606_02218_amd.prof trace DIR [TOP]        # per kernel and grid size, from kernel_trace.csv
+    python -m paper_2606_02218_amd.prof steps DIR              # decode-step time by active-row bucket
     python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
 """
 from __future__ import annotations
@@ -59,6 +60,52 @@ def trace_table(d: str, top: int = 60) -> str:
     return "\n".join(out)
 
 
+def _kname(r) -> str:
+    return _short(r.get("Kernel_Name", "?")).split("(")[0].split("<")[0]
+
+
+def steps_table(d: str) -> str:
+    """Decode steps delimited by k_compact; a step's row bound comes from the
+    grid of its k_decode_rows launch (one 256-thread block per row).  Reports,
+    per row bucket, the steps, GPU-busy and wall span per step, and the busy
+    time per kernel name."""
+    rows = []
+    for f in _find(d, "kernel_trace.csv"):
+        rows += list(csv.DictReader(open(f)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    buckets = collections.OrderedDict((b, None) for b in (16, 32, 64, 128, 256, 384, 512, 1 << 30))
+    acc = {b: {"steps": 0, "busy": 0.0, "span": 0.0, "k": collections.Counter()} for b in buckets}
+    cur, m, t0, busy = collections.Counter(), None, None, 0.0
+    for r in rows:
+        name = _kname(r)
+        s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        if t0 is None:
+            t0 = s0
+        dur = (e0 - s0) / 1e3
+        cur[name] += dur
+        busy += dur
+        if name == "k_decode_rows":
+            m = int(r.get("Grid_Size_X", "0") or 0) // 256
+        if name == "k_compact":
+            if m is not None:
+                b = next(b for b in buckets if m <= b)
+                a = acc[b]
+                a["steps"] += 1
+                a["busy"] += busy
+                a["span"] += (e0 - t0) / 1e3
+                a["k"].update(cur)
+            cur, m, t0, busy = collections.Counter(), None, None, 0.0
+    out = [f"{'rows<=':>8s} {'steps':>6s} {'busy_ms/step':>13s} {'span_ms/step':>13s} {'total_span_s':>13s}  top kernels (us/step)"]
+    for b, a in acc.items():
+        if not a["steps"]:
+            continue
+        n = a["steps"]
+        top = ", ".join(f"{k} {v / n:.0f}" for k, v in a["k"].most_common(6))
+        out.append(f"{b if b < (1 << 30) else 'more':>8} {n:6d} {a['busy'] / n / 1e3:13.3f} {a['span'] / n / 1e3:13.3f} "
+                   f"{a['span'] / 1e6:13.2f}  {top}")
+    return "\n".join(out)
+
+
 def counter_table(d: str, regex: str) -> str:
     pat = re.compile(regex)
     acc = collections.defaultdict(lambda: [0, 0.0])
@@ -82,6 +129,8 @@ if __name__ == "__main__":
         print(stats_table(sys.argv[2]))
     elif len(sys.argv) >= 3 and sys.argv[1] == "trace":
         print(trace_table(sys.argv[2], int(sys.argv[3]) if len(sys.argv) > 3 else 60))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "steps":
+        print(steps_table(sys.argv[2]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
         print(counter_table(sys.argv[2], sys.argv[3]))
     else:
