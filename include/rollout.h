@@ -109,6 +109,13 @@ typedef struct rg_policy rg_policy;  /* opaque: packed weights, KV pool, workspa
 #define RG_FLAG_PROFILE           2  /* time kernel launches with HIP events (the classes in
                                         rg_sampling.profile_kinds, all when it is 0); read
                                         the totals with rg_kernel_times()                */
+#define RG_FLAG_GROUP_PREFIX      4  /* bf16 models: decode steps attend to each prompt's
+                                        full prefix pages once per group (one workgroup per
+                                        prompt, kv head and prefix chunk scores every active
+                                        sibling) instead of row by row.  Results agree up to
+                                        the summation order of the softmax chunks.  Off by
+                                        default: on MI355X the row-by-row pass reads the
+                                        shared pages from L2 and is faster at G = 16.     */
 
 /* Sampling options.  A NULL rg_sampling* means temperature 1, natural EOS, no
  * flags.  Token t of sequence s is argmax_v fp32(z_v/T) + g_v where g_v is the
@@ -209,7 +216,7 @@ int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t
 #define RG_K_RMSNORM    1
 #define RG_K_GEMM_QKV   2
 #define RG_K_QKV_ROPE   3
-#define RG_K_ATTN       4
+#define RG_K_ATTN       4   /* both attention passes: shared prefix and per row */
 #define RG_K_ATTN_MERGE 5
 #define RG_K_GEMM_O     6
 #define RG_K_GEMM_GU    7

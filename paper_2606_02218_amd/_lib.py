@@ -13,7 +13,7 @@ _lib = None
 
 RG_OK, RG_EINVAL, RG_ENOMEM, RG_EHIP, RG_EUNSUPPORTED = 0, -1, -2, -3, -4
 RG_DTYPE_F32, RG_DTYPE_BF16 = 0, 1
-RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE = 1, 2
+RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE, RG_FLAG_GROUP_PREFIX = 1, 2, 4
 KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge", "gemm_o", "gemm_gu", "swiglu",
                 "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup"]
 
@@ -159,12 +159,14 @@ class Policy:
 
     def rollout(self, prompts, G: Sequence[int], max_new: int, seed: int, temperature: float = 1.0,
                 forced_len=None, force_tokens=None, dump_steps: int = 0, share_prefix: bool = True,
-                profile=False, out=None, stream=None):
+                group_prefix_pass: bool = False, profile=False, out=None, stream=None):
         """prompts: device int32 tensor [P, Lp] or a list of 1-D device int32
         tensors.  Returns (tokens [N, max_new], lengths [N], logprobs
         [N, max_new]) and, with dump_steps, the logits [dump_steps, N, V].
         ``profile``: False, True (time every kernel class) or an iterable of
-        class names from KERNEL_KINDS to time."""
+        class names from KERNEL_KINDS to time.  ``group_prefix_pass=True``
+        makes bf16 models attend to each prompt's shared prefix once per group
+        (RG_FLAG_GROUP_PREFIX)."""
         import torch
         lib = load_library()
         if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
@@ -186,7 +188,8 @@ class Policy:
         else:
             tokens, lengths, logprobs = out
         dump = torch.empty((dump_steps, N, self.shape.vocab), dtype=torch.float32, device=dev) if dump_steps else None
-        flags = (0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+        flags = ((0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+                 | (RG_FLAG_GROUP_PREFIX if group_prefix_pass else 0))
         kinds = 0
         if profile and profile is not True:
             for name in profile:

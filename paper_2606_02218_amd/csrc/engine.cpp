@@ -41,8 +41,12 @@ int fail(int code, const std::string& msg) {
 
 constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
 constexpr int RG_SPLIT_MAX = GEMM_MAX_SPLITS;   // largest split-K factor of a decode GEMM
-constexpr int RG_GEMM_TARGET = 512;    // blocks a GEMM launch aims for
+constexpr int RG_GEMM_TARGET = 384;    // blocks a split-K GEMM launch aims for
+constexpr int RG_GEMM_FULL = 256;      // output-tile blocks that need no split
 constexpr int RG_ATT_TARGET = 4096;    // work items an attention launch aims for
+constexpr int RG_PRE_TARGET = 512;     // workgroups the prefix attention pass aims for
+constexpr int RG_PRE_MIN_CHUNK = 64;   // fewest prefix tokens per prefix workgroup
+constexpr int RG_PRE_MAX_SLOTS = 16;   // prefix chunks per row (more only for prefixes > 16k tokens)
 constexpr int RG_RING = 64;            // async active-count slots
 constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
 constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
@@ -88,7 +92,8 @@ struct rg_policy {
           *seq_forced = nullptr, *grp_off = nullptr, *prompt_off = nullptr, *plen = nullptr, *G_dev = nullptr,
           *act_seq = nullptr, *act_tok = nullptr, *done = nullptr, *row_tab = nullptr, *row_pos = nullptr,
           *free_stack = nullptr, *state = nullptr, *copy_pairs = nullptr, *last_rows = nullptr,
-          *hist_active = nullptr, *hist_groups = nullptr;
+          *hist_active = nullptr, *hist_groups = nullptr, *row_beg = nullptr, *grp_row0 = nullptr,
+          *grp_row1 = nullptr;
   int64_t* hist_ctx = nullptr;
   int hist_cap = 0;
 
@@ -181,11 +186,14 @@ struct ProfScope {
 void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits, int* kps) {
   int S = 1;
   if (pol->dtype == RG_DTYPE_BF16) {
+    // Split K only while the output tiles leave the chip short of blocks, and
+    // only as far as the fp32 partials (written once, read once: 8 bytes per
+    // output element and split) stay within twice the weight bytes or 24 MiB.
     const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub), bn = gemm_tile_cols(pol->dtype, rows_ub);
     const int64_t blocks = ceil_div(N, bn) * ceil_div(rows_ub, bm);
-    if (blocks < RG_GEMM_TARGET) S = (int)ceil_div(RG_GEMM_TARGET, blocks);
-    const int64_t budget = std::max<int64_t>(4LL * N * K, 32LL << 20);
-    S = (int)std::min<int64_t>({(int64_t)S, K / 128, budget / (4LL * rows_ub * N), RG_SPLIT_MAX});
+    if (blocks < RG_GEMM_FULL) S = (int)ceil_div(RG_GEMM_TARGET, blocks);
+    const int64_t budget = std::max<int64_t>(4LL * N * K, 24LL << 20);
+    S = (int)std::min<int64_t>({(int64_t)S, K / 128, budget / (8LL * rows_ub * N), RG_SPLIT_MAX});
     S = std::max(1, S);
   }
   const int step = pol->dtype == RG_DTYPE_BF16 ? 64 : 1;
@@ -220,12 +228,24 @@ int gemm(rg_policy* pol, hipStream_t st, int kind, const void* A, int K, const v
   return RG_OK;
 }
 
+// With RG_FLAG_GROUP_PREFIX, decode steps of bf16 models attend to each
+// prompt's full prefix pages once per group (prefix pass) and to the rest per
+// row.
+struct PrefixPass {
+  int P;                // prompts
+  int tab_base;         // page table row of prompt 0 (the rollout's N)
+  int max_group_rows;   // largest G
+  int max_pref;         // largest full-page prefix, (plen / 16) * 16
+};
+
 // The decoder blocks over `rows_ub` rows (actual count at *d_rows), whose
-// row_tab / row_pos are set and whose first attention norm is in pol->abuf;
-// ctx_max bounds every row's context length.  On return pol->abuf holds the
-// final norm of every row (final_norm_rows) or x the residual stream after
-// the last block.
-int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max, bool final_norm_rows) {
+// row_tab / row_pos / row_beg are set and whose first attention norm is in
+// pol->abuf; ctx_max bounds every row's context length.  pre != NULL runs the
+// prefix pass (row_beg then holds each row's prefix length).  On return
+// pol->abuf holds the final norm of every row (final_norm_rows) or x the
+// residual stream after the last block.
+int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max, bool final_norm_rows,
+               const PrefixPass* pre) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
   // chunks per row: enough work items to cover the chip, at least ~256 tokens
@@ -234,7 +254,18 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
   if ((int64_t)rows_ub * pol->nkv < RG_ATT_TARGET)
     n_chunks = (int)std::min<int64_t>(ceil_div(RG_ATT_TARGET, (int64_t)rows_ub * pol->nkv), ceil_div(ctx_max, 256));
   n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16000)});
-  if ((int64_t)rows_ub * n_chunks > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
+  AttPlan plan{n_chunks, 0, 0, n_chunks};
+  if (pre && pre->max_pref > 0) {
+    // prefix chunks: about RG_PRE_TARGET workgroups, at least RG_PRE_MIN_CHUNK
+    // tokens and at most 1024 tokens each
+    int slots = (int)std::min<int64_t>({ceil_div(RG_PRE_TARGET, (int64_t)pol->nkv * pre->P),
+                                        ceil_div(pre->max_pref, RG_PRE_MIN_CHUNK), RG_PRE_MAX_SLOTS});
+    slots = std::max<int>({1, slots, (int)ceil_div(pre->max_pref, 1024)});
+    plan.pre_chunk = (int)ceil_div(ceil_div(pre->max_pref, slots), 32) * 32;
+    plan.pre_slots = (int)ceil_div(pre->max_pref, plan.pre_chunk);
+    plan.n_slots = plan.pre_slots + n_chunks;
+  }
+  if ((int64_t)rows_ub * plan.n_slots > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
   const float eps = pol->cfg.rms_eps;
   GemmEpi qkv{};
   qkv.mode = GEMM_EPI_QKV;
@@ -252,11 +283,16 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     qkv.layer = l;
     if ((rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, d_rows, rows_ub, qkv)))
       return rc;
+    if (plan.pre_slots)
+      LAUNCH(RG_K_ATTN, launch_attention_prefix(pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
+                                                pol->page_tab, tab_stride, pre->tab_base, pol->plen,
+                                                pol->grp_row0, pol->grp_row1, pre->P, pre->max_group_rows, plan,
+                                                pol->att_o, pol->att_ml, st));
     LAUNCH(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
-                                       pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, ctx_max, n_chunks,
-                                       pol->att_o, pol->att_ml, d_rows, rows_ub, st));
+                                       pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, pol->row_beg, ctx_max,
+                                       plan, pol->att_o, pol->att_ml, d_rows, rows_ub, st));
     LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
-                                              n_chunks, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+                                              pol->row_beg, plan, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
     // O projection + residual, then the MLP norm into abuf (fused into the
     // split epilogue when K is split)
     int S;
@@ -309,15 +345,16 @@ int sample_slices(int rows_ub) {
 }
 
 // Every kernel of one decode step (t >= 1, read on the device from state[8]).
-int enqueue_step(rg_policy* pol, hipStream_t st, int rows_ub, int ctx_max, SampleArgs sm, const CompactArgs& ca) {
+int enqueue_step(rg_policy* pol, hipStream_t st, int rows_ub, int ctx_max, SampleArgs sm, const CompactArgs& ca,
+                 const PrefixPass* pre) {
   sm.n_slices = sample_slices(rows_ub);
   int rc;
   LAUNCH(RG_K_EMBED, launch_decode_rows(pol->dtype, pol->w_embed, pol->d, pol->act_seq, pol->act_tok, pol->seq_grp,
-                                        pol->plen, pol->state + 8, pol->row_tab, pol->row_pos, pol->x, pol->state,
-                                        rows_ub, st));
+                                        pol->plen, pol->state + 8, pre ? 1 : 0, pol->row_tab, pol->row_pos,
+                                        pol->row_beg, pol->x, pol->state, rows_ub, st));
   LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
                                        pol->a_plane, nullptr, pol->state, rows_ub, st));
-  if ((rc = run_layers(pol, st, pol->state, rows_ub, ctx_max, true))) return rc;
+  if ((rc = run_layers(pol, st, pol->state, rows_ub, ctx_max, true, pre))) return rc;
   if ((rc = run_head(pol, st, pol->state, rows_ub, nullptr))) return rc;
   LAUNCH(RG_K_SAMPLE, launch_sample(sm, rows_ub, st));
   LAUNCH(RG_K_COMPACT, launch_compact(ca, st));
@@ -333,11 +370,11 @@ struct StepGraphs {
 };
 
 int step_graph(rg_policy* pol, StepGraphs& gs, int rows_ub, int ctx_max, const SampleArgs& sm,
-               const CompactArgs& ca, hipGraphExec_t* out) {
+               const CompactArgs& ca, const PrefixPass* pre, hipGraphExec_t* out) {
   for (auto& g : gs.execs)
     if (g.first == rows_ub) { *out = g.second; return RG_OK; }
   HIPTRY(hipStreamBeginCapture(pol->cap_st, hipStreamCaptureModeThreadLocal));
-  const int rc = enqueue_step(pol, pol->cap_st, rows_ub, ctx_max, sm, ca);
+  const int rc = enqueue_step(pol, pol->cap_st, rows_ub, ctx_max, sm, ca, pre);
   hipGraph_t graph = nullptr;
   const hipError_t e = hipStreamEndCapture(pol->cap_st, &graph);
   if (rc) {
@@ -494,7 +531,8 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   const int64_t M = pol->m_act, S = lim.max_seqs, P = lim.max_prompts;
   const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
   pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
-  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + RG_ATT_TARGET;
+  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + RG_ATT_TARGET +
+                       S * (RG_PRE_MAX_SLOTS + ceil_div(lim.max_context, 1024));
   pol->hist_cap = lim.max_context;
   struct Piece { void** p; size_t bytes; };
   const int64_t kmax = std::max<int64_t>({d, pol->q_dim, pol->F});
@@ -524,6 +562,9 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       {(void**)&pol->done, (size_t)(S * 4)},
       {(void**)&pol->row_tab, (size_t)(M * 4)},
       {(void**)&pol->row_pos, (size_t)(M * 4)},
+      {(void**)&pol->row_beg, (size_t)(M * 4)},
+      {(void**)&pol->grp_row0, (size_t)(P * 4)},
+      {(void**)&pol->grp_row1, (size_t)(P * 4)},
       {(void**)&pol->free_stack, (size_t)(pol->pool_pages * 4)},
       {(void**)&pol->state, 64},
       {(void**)&pol->copy_pairs, (size_t)(2 * S * pol->max_pages * 4)},
@@ -637,12 +678,13 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
 
   // ---- prefill
   const int* d_pre = pol->state + 5;
-  LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, Ni, pol->row_tab, pol->row_pos, (int)T_pre, st));
+  LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, Ni, pol->row_tab, pol->row_pos, pol->row_beg,
+                                         (int)T_pre, st));
   LAUNCH(RG_K_EMBED, launch_embed(pol->dtype, pol->w_embed, pol->d, pol->V, prompts, pol->x, pol->state + 7, d_pre,
                                   (int)T_pre, st));
   LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
                                        pol->a_plane, nullptr, d_pre, (int)T_pre, st));
-  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen, false);
+  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen, false, nullptr);
   if (rc) return rc;
   rc = run_head(pol, st, pol->state + 6, P, pol->last_rows);
   if (rc) return rc;
@@ -679,6 +721,18 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   ca.plen = pol->plen; ca.page_tab = pol->page_tab; ca.seq_npages = pol->seq_npages; ca.seq_nshared = pol->seq_nshared;
   ca.free_stack = pol->free_stack; ca.state = pol->state; ca.lengths = lengths; ca.hist_active = pol->hist_active;
   ca.hist_groups = pol->hist_groups; ca.hist_ctx = pol->hist_ctx; ca.hist_cap = pol->hist_cap;
+  ca.P = P; ca.grp_row0 = pol->grp_row0; ca.grp_row1 = pol->grp_row1;
+
+  // shared-prefix attention pass of the decode steps
+  PrefixPass pp{};
+  pp.P = P;
+  pp.tab_base = Ni;
+  for (int p = 0; p < P; ++p) {
+    pp.max_group_rows = std::max(pp.max_group_rows, G[p]);
+    pp.max_pref = std::max(pp.max_pref, prompt_len[p] / pol->page_tok * pol->page_tok);
+  }
+  const PrefixPass* pre =
+      pol->dtype == RG_DTYPE_BF16 && (o.flags & RG_FLAG_GROUP_PREFIX) && pp.max_pref > 0 ? &pp : nullptr;
 
   auto snapshot = [&](int t) -> int {
     const int slot = t % RG_RING;
@@ -724,10 +778,10 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
     const int rows_ub = std::min(row_bucket(m_ub), pol->m_act);
     if (graphs_on) {
       hipGraphExec_t exec;
-      if ((rc = step_graph(pol, graphs, rows_ub, ctx_all, sm, ca, &exec))) return rc;
+      if ((rc = step_graph(pol, graphs, rows_ub, ctx_all, sm, ca, pre, &exec))) return rc;
       HIPTRY(hipGraphLaunch(exec, st));
     } else {
-      if ((rc = enqueue_step(pol, st, rows_ub, ctx_all, sm, ca))) return rc;
+      if ((rc = enqueue_step(pol, st, rows_ub, ctx_all, sm, ca, pre))) return rc;
     }
     if ((rc = snapshot(t))) return rc;
     last_t = t;

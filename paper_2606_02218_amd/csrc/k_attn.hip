@@ -1,10 +1,18 @@
 // Paged causal attention over the KV pool, for prefill rows and decode rows
-// alike.  Work item = (row, kv head, chunk of the row's context); it keeps a
-// running softmax (max, sum) and an unnormalised output per query head of the
-// GQA group, and the merge kernel combines the chunks.  Context positions
-// 0..row_pos[r] of page table row_tab[r]; position j lives in page
-// page_tab[tab*tab_stride + j/page_tok], slot j % page_tok.  Inside a page a
-// layer holds K as [kv head][slot][dim] and V transposed, [kv head][dim][slot].
+// alike.  Row r attends to positions 0..row_pos[r] through page table
+// row_tab[r]; position j lives in page page_tab[tab*tab_stride + j/16], slot
+// j % 16.  Inside a page a layer holds K as [kv head][slot][dim] and V
+// transposed, [kv head][dim][slot].  Every work item keeps a running softmax
+// (max, sum) and an unnormalised output per query head of its GQA group in a
+// partial slot of the row; the merge kernel combines a row's slots.
+//
+// Decode rows split their context in two.  The prompt's full pages (positions
+// 0..row_beg[r]-1, shared by all siblings of the prompt) go through the
+// prefix kernel: one workgroup per (prompt, kv head, prefix chunk) stages
+// each 32-token block of K and V^T once in LDS and scores it against the
+// query rows of every active sibling (siblings x GQA heads rows, 16 per
+// wave).  The rest (row_beg[r]..row_pos[r]: the copied partial page and the
+// sequence's own tokens) goes through the per-row kernel.
 //
 // bf16 KV: one wave per work item on MFMA 16x16x32.  Scores are formed
 // transposed, S^T = K Q^T (tokens x query heads), so each lane ends up holding
@@ -56,14 +64,15 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
                                                    const int32_t* __restrict__ page_tab, int tab_stride,
                                                    const int32_t* __restrict__ row_tab,
                                                    const int32_t* __restrict__ row_pos,
-                                                   int n_chunks, float* __restrict__ part_o,
-                                                   float* __restrict__ part_ml, const int* __restrict__ d_rows) {
+                                                   const int32_t* __restrict__ row_beg, AttPlan plan,
+                                                   float* __restrict__ part_o, float* __restrict__ part_ml,
+                                                   const int* __restrict__ d_rows) {
   const int r = blockIdx.z;
   if (r >= *d_rows) return;
   const int kvh = blockIdx.y, chunk = blockIdx.x;
-  const int ctx = row_pos[r] + 1;
-  const int clen = att_chunk_len(ctx, n_chunks);
-  const int c0 = chunk * clen;
+  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
+  const int c0 = beg + chunk * clen;
   if (c0 >= ctx) return;
   const int c1 = min(ctx, c0 + clen);
   const int rep = n_q / n_kv;
@@ -83,7 +92,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
   const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * g.page_tok * hd;   // V^T [dim][slot]
 
   // each thread owns output slots (h, d) = idx / hd, idx % hd for idx = tid + 256*k
-  const int n_slots = (rep * hd + 255) / 256;
+  const int n_own = (rep * hd + 255) / 256;
   float acc[ATT_MAX_REP];
 #pragma unroll
   for (int k = 0; k < ATT_MAX_REP; ++k) acc[k] = 0.f;
@@ -131,7 +140,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     }
     __syncthreads();
     // ---- accumulate p * V
-    for (int k = 0; k < n_slots; ++k) {
+    for (int k = 0; k < n_own; ++k) {
       const int idx = tid + 256 * k;
       if (idx < rep * hd) {
         const int h = idx / hd, d = idx % hd;
@@ -147,8 +156,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     __syncthreads();
   }
   // ---- write partials
-  const int64_t base = ((int64_t)r * n_chunks + chunk) * n_q + kvh * rep;
-  for (int k = 0; k < n_slots; ++k) {
+  const int64_t base = ((int64_t)r * plan.n_slots + plan.pre_slots + chunk) * n_q + kvh * rep;
+  for (int k = 0; k < n_own; ++k) {
     const int idx = tid + 256 * k;
     if (idx < rep * hd) part_o[base * hd + idx] = acc[k];
   }
@@ -160,14 +169,14 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
 
 
 // ---------------------------------------------------------------- MFMA path
+// Eight fp32 values as hi = bf16(v) and lo = bf16(v - hi) fragments
+// (v_cvt_pk_bf16_f32 rounds to nearest even; v - hi is exact in fp32).
 __device__ __forceinline__ void split8(const float* v, bf16x8_t& hi, bf16x8_t& lo) {
   uint32_t h[4], l[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const bf16_t h0 = f32_to_bf16(v[2 * i]), h1 = f32_to_bf16(v[2 * i + 1]);
-    const bf16_t l0 = f32_to_bf16(v[2 * i] - bf16_to_f32(h0)), l1 = f32_to_bf16(v[2 * i + 1] - bf16_to_f32(h1));
-    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    h[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    l[i] = pack_bf16x2(v[2 * i] - __uint_as_float(h[i] << 16), v[2 * i + 1] - __uint_as_float(h[i] & 0xFFFF0000u));
   }
   hi = __builtin_bit_cast(bf16x8_t, uint4{h[0], h[1], h[2], h[3]});
   lo = __builtin_bit_cast(bf16x8_t, uint4{l[0], l[1], l[2], l[3]});
@@ -178,6 +187,134 @@ constexpr int ATT_MAX_MERGE = 1024;         // chunks per row
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+// Scores are kept in log2 units (q is pre-scaled by log2(e) / sqrt(hd)), so
+// probabilities are exp2(s - m).  The running max m may lag the true max by up
+// to ATT_SLACK (probabilities then reach 2^ATT_SLACK, far from fp32 overflow):
+// the accumulators are rescaled only when a score exceeds m + ATT_SLACK,
+// which after the first blocks of a row is rare.  Softmax does not depend on
+// the constant subtracted, so only rounding changes.
+constexpr float ATT_SLACK = 8.f;
+constexpr float ATT_LN2 = 0.693147180559945309f;
+constexpr float ATT_LOG2E = 1.44269504088896341f;
+
+// Online-softmax state of one wave: column `col` of the lane is one query
+// row; O^T rows 4*grp .. +3 of every 16-dim tile dt.
+template <int HD>
+struct AttState {
+  float m, l;
+  f32x4_t o[HD / 16];
+};
+
+// Scores S^T of one 32-token block for the lane's query column: s[tt][j] is
+// token 8*grp + 4*tt + j of the block.  K fragments kf(tt, kb) supply row
+// col of tile tt, dims kb*32 + 8*grp .. +7.
+template <int HD, typename KFrag>
+__device__ __forceinline__ void att_scores(f32x4_t (&s)[2], const bf16x8_t (&qh)[HD / 32],
+                                           const bf16x8_t (&ql)[HD / 32], KFrag kf) {
+  f32x4_t a0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, a1 = a0;
+#pragma unroll
+  for (int kb = 0; kb < HD / 32; ++kb) {   // two independent accumulation chains
+    const bf16x8_t k0 = kf(0, kb), k1 = kf(1, kb);
+    a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qh[kb], a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qh[kb], a1, 0, 0, 0);
+    a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, ql[kb], a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, ql[kb], a1, 0, 0, 0);
+  }
+  s[0] = a0;
+  s[1] = a1;
+}
+
+// Softmax update and O^T += V^T P^T for one block.  nval = valid tokens among
+// the lane group's 8 (only the last block of a range has fewer: `tail`).
+// V fragments vf(dt) hold dims dt*16 + col, the lane group's 8 tokens.
+template <int HD, typename VFrag>
+__device__ __forceinline__ void att_update(AttState<HD>& st, f32x4_t (&s)[2], bool tail, int nval, VFrag vf) {
+  if (tail) {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * tt + j >= nval) s[tt][j] = -INFINITY;
+  }
+  float mloc = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                     fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+  if (__any(mloc > st.m + ATT_SLACK)) {
+    const float m_new = fmaxf(st.m, mloc);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);   // 0 on the first block (m = -inf)
+    st.l *= alpha;
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) st.o[i] *= alpha;
+    st.m = m_new;
+  }
+  float p[8];
+  float psum = 0.f;
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float e = __builtin_amdgcn_exp2f(s[tt][j] - st.m);   // exp2(-inf) = 0 for masked tokens
+      p[tt * 4 + j] = e;
+      psum += e;
+    }
+  psum += __shfl_xor(psum, 16, 64);
+  psum += __shfl_xor(psum, 32, 64);
+  st.l += psum;
+  bf16x8_t ph, pl;
+  split8(p, ph, pl);
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) {
+    u32x4_t vv = vf(dt);
+    if (tail) {   // zero the slots of masked tokens (their memory may hold anything)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n2 = nval - 2 * e;   // valid tokens in this dword
+        vv[e] = n2 >= 2 ? vv[e] : (n2 == 1 ? (vv[e] & 0xFFFFu) : 0u);
+      }
+    }
+    const bf16x8_t v8 = __builtin_bit_cast(bf16x8_t, vv);
+    st.o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v8, ph, st.o[dt], 0, 0, 0);
+    st.o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v8, pl, st.o[dt], 0, 0, 0);
+  }
+}
+
+// Q^T fragments of one query row (a lane's column): dims kb*32 + 8*grp .. +7,
+// scaled by log2(e) / sqrt(HD) and split into hi/lo planes.  valid = false
+// gives zeros (padding columns; qr must still point at a readable row).
+template <int HD>
+__device__ __forceinline__ void att_load_q(const float* __restrict__ qr, bool valid, int grp,
+                                           bf16x8_t (&qh)[HD / 32], bf16x8_t (&ql)[HD / 32]) {
+  const float scale = valid ? ATT_LOG2E / sqrtf((float)HD) : 0.f;
+  f32x4_t x[HD / 32][2];   // every load issued before the first conversion
+#pragma unroll
+  for (int kb = 0; kb < HD / 32; ++kb) {
+    x[kb][0] = *reinterpret_cast<const f32x4_t*>(qr + kb * 32 + 8 * grp);
+    x[kb][1] = *reinterpret_cast<const f32x4_t*>(qr + kb * 32 + 8 * grp + 4);
+  }
+#pragma unroll
+  for (int kb = 0; kb < HD / 32; ++kb) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { v[i] = x[kb][0][i] * scale; v[4 + i] = x[kb][1][i] * scale; }
+    split8(v, qh[kb], ql[kb]);
+  }
+}
+
+// The partial of one (row, head, slot): O unnormalised, (m, l) with m in
+// natural-log units as the merge expects.
+template <int HD>
+__device__ __forceinline__ void att_store(const AttState<HD>& st, int64_t base, int grp, float* __restrict__ part_o,
+                                          float* __restrict__ part_ml) {
+  float* po = part_o + base * HD + 4 * grp;
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) *reinterpret_cast<f32x4_t*>(po + dt * 16) = st.o[dt];
+  if (grp == 0) {
+    part_ml[base * 2] = st.m * ATT_LN2;
+    part_ml[base * 2 + 1] = st.l;
+  }
+}
+
 // Registers of one 32-token block: K fragments of both 16-token tiles and the
 // V^T fragments of every 16-dim output tile.
 template <int HD>
@@ -186,21 +323,22 @@ struct AttBlock {
   u32x4_t v[HD / 16];
 };
 
+// K: A-fragment row i of tile tt is token t0 + 8*(i/4) + 4*tt + (i%4), so that
+// the S^T layout leaves lane group grp holding tokens t0+8*grp .. +7; the
+// lane's two rows share one page.  V^T: dims dt*16 + col, tokens t0+8*grp ..
+// +7 (one page slot run).  Tokens past c1 read token c0 instead (masked).
 template <int HD>
 __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restrict__ pool, const KvGeom& g,
                                          int64_t koff, int64_t voff, const int* spg, int c0, int c1, int t0,
                                          int col, int grp) {
-  // K: A-fragment row i of tile tt is token t0 + 8*(i/4) + 4*tt + (i%4), so that
-  // the S^T layout leaves lane group grp holding tokens t0+8*grp .. +7
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     int tok = t0 + 8 * (col >> 2) + 4 * tt + (col & 3);
-    if (tok >= c1) tok = c0;                 // keep the load in bounds; masked later
+    if (tok >= c1) tok = c0;
     const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff + (int64_t)(tok & 15) * HD + 8 * grp;
 #pragma unroll
     for (int kb = 0; kb < HD / 32; ++kb) b.k[tt][kb] = *reinterpret_cast<const u32x4_t*>(kp + kb * 32);
   }
-  // V^T: lane reads dims (dt*16 + col), tokens t0+8*grp .. +7 (one page slot run)
   const int tv = t0 + 8 * grp;
   const int pg = spg[((tv < c1 ? tv : c0) - c0) >> 4];
   const bf16_t* vp = pool + (int64_t)pg * g.page_elems + voff + (tv & 15);
@@ -209,18 +347,20 @@ __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restri
 }
 
 template <int HD>
-__global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
+__global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
                                                        const bf16_t* __restrict__ pool, KvGeom g, int layer,
                                                        const int32_t* __restrict__ page_tab, int tab_stride,
                                                        const int32_t* __restrict__ row_tab,
                                                        const int32_t* __restrict__ row_pos,
-                                                       int n_chunks, int rows_ub, float* __restrict__ part_o,
+                                                       const int32_t* __restrict__ row_beg, AttPlan plan,
+                                                       int rows_ub, float* __restrict__ part_o,
                                                        float* __restrict__ part_ml, const int* __restrict__ d_rows) {
   static_assert(HD % 32 == 0 && HD <= 256, "head_dim");
   // XCD-aware order: the 1-D grid has a multiple of 8 blocks and blocks are
   // dealt to the 8 XCDs round-robin, so XCD x = b % 8 takes the contiguous
   // work range [x*per_xcd, (x+1)*per_xcd): neighbouring rows (siblings of one
   // prompt) share an XCD, whose L2 then holds their shared prefix.
+  const int n_chunks = plan.n_chunks;
   const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
   const int64_t b = blockIdx.x;
   const int64_t per_xcd = (int64_t)gridDim.x / 8;
@@ -230,9 +370,9 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
   const int kvh = (int)((w / n_chunks) % n_kv);
   const int r = (int)(w / ((int64_t)n_chunks * n_kv));
   if (r >= *d_rows) return;
-  const int ctx = row_pos[r] + 1;
-  const int clen = att_chunk_len(ctx, n_chunks);
-  const int c0 = chunk * clen;
+  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  const int clen = att_chunk_len(ctx - beg, n_chunks);
+  const int c0 = beg + chunk * clen;                // a multiple of 16
   if (c0 >= ctx) return;
   const int c1 = min(ctx, c0 + clen);
   const int rep = n_q / n_kv;
@@ -246,127 +386,196 @@ __global__ __launch_bounds__(64) void k_attention_mfma(const float* __restrict__
     for (int i = lane; i < npg; i += 64) spg[i] = tab[i];
     __syncthreads();
   }
-  // Q^T fragments: lane holds q[head col][kb*32 + 8*grp + 0..7], pre-scaled by 1/sqrt(hd)
-  bf16x8_t qh[HD / 32], ql[HD / 32];
+  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
+  AttBlock<HD> ba, bb;
+  att_load<HD>(ba, pool, g, koff, voff, spg, c0, c1, c0, col, grp);   // first block in flight during the q set-up
+  // Q^T fragments (lanes >= rep: zero padding columns), parked in LDS in lane
+  // order so that each lane reads back its own 16-byte pieces
+  __shared__ __attribute__((aligned(16))) u32x4_t sq[2][HD / 32][64];
   {
-    const float scale = 1.0f / sqrtf((float)HD);
-    const float* qr = q + ((int64_t)r * n_q + kvh * rep + min(col, rep - 1)) * HD + 8 * grp;   // lanes >= rep: padding
+    bf16x8_t qh[HD / 32], ql[HD / 32];
+    att_load_q<HD>(q + ((int64_t)r * n_q + kvh * rep + min(col, rep - 1)) * HD, col < rep, grp, qh, ql);
 #pragma unroll
     for (int kb = 0; kb < HD / 32; ++kb) {
-      float v[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = col < rep ? qr[kb * 32 + i] * scale : 0.f;
-      split8(v, qh[kb], ql[kb]);
+      sq[0][kb][lane] = __builtin_bit_cast(u32x4_t, qh[kb]);
+      sq[1][kb][lane] = __builtin_bit_cast(u32x4_t, ql[kb]);
     }
   }
+
+  AttState<HD> st;
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int i = 0; i < HD / 16; ++i) st.o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // two register blocks in turn: the next block's loads are in flight while
+  // the current one is multiplied out
+  auto step = [&](const AttBlock<HD>& blk, int t0) {
+    f32x4_t s[2];
+    bf16x8_t qh[HD / 32], ql[HD / 32];
+    asm volatile("" ::: "memory");   // re-read q from LDS each block rather than pinning it in registers
+#pragma unroll
+    for (int kb = 0; kb < HD / 32; ++kb) {
+      qh[kb] = __builtin_bit_cast(bf16x8_t, sq[0][kb][lane]);
+      ql[kb] = __builtin_bit_cast(bf16x8_t, sq[1][kb][lane]);
+    }
+    att_scores<HD>(s, qh, ql, [&](int tt, int kb) { return __builtin_bit_cast(bf16x8_t, blk.k[tt][kb]); });
+    att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))), [&](int dt) { return blk.v[dt]; });
+  };
+  for (int t0 = c0; t0 < c1; t0 += 64) {
+    if (t0 + 32 < c1) att_load<HD>(bb, pool, g, koff, voff, spg, c0, c1, t0 + 32, col, grp);
+    step(ba, t0);
+    if (t0 + 32 >= c1) break;
+    if (t0 + 64 < c1) att_load<HD>(ba, pool, g, koff, voff, spg, c0, c1, t0 + 64, col, grp);
+    step(bb, t0 + 32);
+  }
+  if (col < rep)
+    att_store<HD>(st, ((int64_t)r * plan.n_slots + plan.pre_slots + chunk) * n_q + kvh * rep + col, grp, part_o,
+                  part_ml);
+}
+
+
+// Prefix pass.  Workgroup (chunk, kv head, prompt p, row block b) with W
+// waves; wave w scores query rows 16(bW + w) .. +15 of the group (row i =
+// sibling i / rep, GQA head i % rep).
+// Per 32-token block every thread stages a few 16-byte pieces of K (LDS row
+// = the fragment lane order of S^T, so one quarter-wave reads 16 consecutive
+// rows) and V^T (padded rows) for the next block in registers while the
+// waves multiply the current block out of LDS (two LDS buffers).
+constexpr int ATT_PRE_MAX_WAVES = 8;
+
+template <int HD>
+__global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(const float* __restrict__ q, int n_q, int n_kv,
+                                                         const bf16_t* __restrict__ pool, KvGeom g, int layer,
+                                                         const int32_t* __restrict__ page_tab, int tab_stride,
+                                                         int tab_base, const int32_t* __restrict__ plen,
+                                                         const int32_t* __restrict__ grp_row0,
+                                                         const int32_t* __restrict__ grp_row1, int n_rblk,
+                                                         AttPlan plan, float* __restrict__ part_o,
+                                                         float* __restrict__ part_ml) {
+  constexpr int KROW = HD + 8;                  // LDS row stride of K (elements)
+  constexpr int VROW = 40;                      // LDS row stride of V^T (32 tokens + 8)
+  constexpr int PIECES = 8 * HD;                // 16-byte pieces per block: K 4*HD, V^T 4*HD
+  constexpr int MAXP = PIECES / 256;            // pieces per thread (at least 4 waves)
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][32 * KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VROW];
+  __shared__ int spg[64];
+
+  const int c = blockIdx.x, kvh = blockIdx.y, p = blockIdx.z / n_rblk, rb = blockIdx.z % n_rblk;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nthr = blockDim.x;
+  const int r0 = grp_row0[p], r1 = grp_row1[p];
+  const int rep = n_q / n_kv;
+  const int q0 = rb * (nthr / 4);                // first query row of this block (16 per wave)
+  const int nrows = (r1 - r0) * rep;
+  if (q0 >= nrows) return;
+  const int pref = (plen[p] >> 4) << 4;
+  const int c0 = c * plan.pre_chunk;
+  if (c0 >= pref) return;
+  const int c1 = min(pref, c0 + plan.pre_chunk);
+  const int col = lane & 15, grp = lane >> 4;
+  const bool active = q0 + wave * 16 < nrows;
+  const int qi = q0 + wave * 16 + col;
+  const bool qv = qi < nrows;
+  const int row = r0 + (qv ? qi / rep : 0), head = kvh * rep + (qv ? qi % rep : 0);
+
+  {
+    const int32_t* tab = page_tab + (int64_t)(tab_base + p) * tab_stride + (c0 >> 4);
+    const int npg = (c1 - c0 + 15) >> 4;
+    for (int i = tid; i < npg; i += nthr) spg[i] = tab[i];
+  }
+  bf16x8_t qh[HD / 32], ql[HD / 32];
+  att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
+  __syncthreads();   // page ids
   const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
   const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
 
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t oacc[HD / 16];
+  u32x4_t rg[MAXP];
+  auto fetch = [&](int t0) {
 #pragma unroll
-  for (int i = 0; i < HD / 16; ++i) oacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  AttBlock<HD> cur, nxt;
-  att_load<HD>(cur, pool, g, koff, voff, spg, c0, c1, c0, col, grp);
-  for (int t0 = c0; t0 < c1; t0 += 32) {
-    if (t0 + 32 < c1) att_load<HD>(nxt, pool, g, koff, voff, spg, c0, c1, t0 + 32, col, grp);   // next block in flight
-    // ---- S^T = K Q^T; lane holds tokens t0 + 8*grp + 4*tt + j of query head col
-    f32x4_t s[2];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < HD / 32; ++kb) {
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, cur.k[tt][kb]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[kb], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[kb], acc, 0, 0, 0);
-      }
-      s[tt] = acc;
-    }
-    const int nval = min(8, max(0, c1 - (t0 + 8 * grp)));   // valid tokens among this lane group's 8
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (4 * tt + j >= nval) s[tt][j] = -INFINITY;
-        mloc = fmaxf(mloc, s[tt][j]);
-      }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = expf(m_run - m_new);       // 0 on the first block
-    float p[8];
-    float psum = 0.f;
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float e = expf(s[tt][j] - m_new);    // exp(-inf) = 0 for masked tokens
-        p[tt * 4 + j] = e;
-        psum += e;
-      }
-    psum += __shfl_xor(psum, 16, 64);
-    psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < HD / 16; ++i) oacc[i] *= alpha;
-    bf16x8_t ph, pl;
-    split8(p, ph, pl);
-    // ---- O^T += V^T P^T (k = this lane group's 8 tokens, in order)
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) {
-      u32x4_t vv = cur.v[dt];
-      if (nval < 8) {   // zero the slots of masked tokens (their memory may hold anything)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int n2 = nval - 2 * e;   // valid tokens in this dword
-          vv[e] = n2 >= 2 ? vv[e] : (n2 == 1 ? (vv[e] & 0xFFFFu) : 0u);
+    for (int k = 0; k < MAXP; ++k) {
+      const int pc = tid + k * nthr;
+      if (pc < PIECES) {
+        if (pc < 4 * HD) {                       // K: token tk, 8 dims from ck*8
+          const int tk = pc / (HD / 8), ck = pc % (HD / 8);
+          int tok = t0 + tk;
+          if (tok >= c1) tok = c0;
+          rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff +
+                                                    (int64_t)(tok & 15) * HD + ck * 8);
+        } else {                                 // V^T: dim dd, tokens q4*8 .. +7
+          const int pv = pc - 4 * HD, dd = pv >> 2, q4 = pv & 3;
+          int tv = t0 + q4 * 8;
+          if (tv >= c1) tv = c0;
+          rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tv - c0) >> 4] * g.page_elems + voff +
+                                                    (int64_t)dd * 16 + (tv & 15));
         }
       }
-      const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, vv);
-      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, oacc[dt], 0, 0, 0);
-      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, oacc[dt], 0, 0, 0);
     }
-    cur = nxt;
-  }
-  // ---- partials: lane holds O^T[dims dt*16 + 4*grp + j][head col]
-  if (col < rep) {
-    const int64_t base = ((int64_t)r * n_chunks + chunk) * n_q + kvh * rep + col;
-    float* po = part_o + base * HD;
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) po[dt * 16 + 4 * grp + j] = oacc[dt][j];
-    if (grp == 0) {
-      part_ml[base * 2] = m_run;
-      part_ml[base * 2 + 1] = l_run;
+    for (int k = 0; k < MAXP; ++k) {
+      const int pc = tid + k * nthr;
+      if (pc < PIECES) {
+        if (pc < 4 * HD) {
+          const int tk = pc / (HD / 8), ck = pc % (HD / 8);
+          const int lrow = 16 * ((tk >> 2) & 1) + (((tk >> 3) << 2) | (tk & 3));   // fragment lane order
+          *reinterpret_cast<u32x4_t*>(&sK[buf][lrow * KROW + ck * 8]) = rg[k];
+        } else {
+          const int pv = pc - 4 * HD, dd = pv >> 2, q4 = pv & 3;
+          *reinterpret_cast<u32x4_t*>(&sV[buf][dd * VROW + q4 * 8]) = rg[k];
+        }
+      }
     }
+  };
+
+  AttState<HD> st;
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int i = 0; i < HD / 16; ++i) st.o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  fetch(c0);
+  int buf = 0;
+  for (int t0 = c0; t0 < c1; t0 += 32, buf ^= 1) {
+    stash(buf);
+    __syncthreads();                             // block t0 in LDS; the other buffer is free
+    if (t0 + 32 < c1) fetch(t0 + 32);
+    if (!active) continue;
+    f32x4_t s[2];
+    const bf16_t* kb0 = &sK[buf][col * KROW + 8 * grp];
+    att_scores<HD>(s, qh, ql, [&](int tt, int kb) {
+      return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kb0 + 16 * tt * KROW + kb * 32));
+    });
+    const bf16_t* vb0 = &sV[buf][col * VROW + 8 * grp];
+    att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))),
+                   [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
   }
+  if (active && qv) att_store<HD>(st, ((int64_t)row * plan.n_slots + c) * n_q + head, grp, part_o, part_ml);
 }
 
 template <int SPLIT>
 __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __restrict__ part_ml, int n_q, int hd,
-                             const int32_t* __restrict__ row_pos, int n_chunks, ActOut out,
-                             const int* __restrict__ d_rows) {
+                             const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_beg,
+                             AttPlan plan, ActOut out, const int* __restrict__ d_rows) {
   const int r = blockIdx.x;
   if (r >= *d_rows) return;
   const int h = blockIdx.y;
-  const int ctx = row_pos[r] + 1;
-  const int clen = att_chunk_len(ctx, n_chunks);
-  const int nc = (ctx + clen - 1) / clen;   // chunks holding context
-  __shared__ float sw[ATT_MAX_MERGE];       // chunk weights exp(m_c - M) / L
-  // (max, sum) of every chunk: one thread per chunk, then a wave reduction
-  const int64_t rb = (int64_t)r * n_chunks;
+  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
+  const int npre = plan.pre_slots ? (beg + plan.pre_chunk - 1) / plan.pre_chunk : 0;   // prefix slots written
+  const int nc = npre + (ctx - beg + clen - 1) / clen;                                  // slots holding context
+  __shared__ float sw[ATT_MAX_MERGE];       // slot weights exp(m_c - M)
+  // slot c of the merge: prefix slot c < npre, else private slot pre_slots + c - npre
+  const int gap = plan.pre_slots - npre;
+  const int64_t rb = (int64_t)r * plan.n_slots;
+#define RG_SLOT(c) ((c) < npre ? (c) : (c) + gap)
   float m = -INFINITY;
-  for (int c = threadIdx.x; c < nc; c += blockDim.x) m = fmaxf(m, part_ml[((rb + c) * n_q + h) * 2]);
+  for (int c = threadIdx.x; c < nc; c += blockDim.x) m = fmaxf(m, part_ml[((rb + RG_SLOT(c)) * n_q + h) * 2]);
   __shared__ float red[16];
   const float M = block_max(m, red);
   float l = 0.f;
   for (int c = threadIdx.x; c < nc; c += blockDim.x) {
-    const float* ml = part_ml + ((rb + c) * n_q + h) * 2;
+    const float* ml = part_ml + ((rb + RG_SLOT(c)) * n_q + h) * 2;
     const float w = expf(ml[0] - M);
     sw[c] = w;
     l += w * ml[1];
@@ -376,23 +585,26 @@ __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __re
     float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;   // independent sums keep several loads in flight
     int c = 0;
     for (; c + 4 <= nc; c += 4) {
-      o0 += sw[c] * part_o[((rb + c) * n_q + h) * hd + d];
-      o1 += sw[c + 1] * part_o[((rb + c + 1) * n_q + h) * hd + d];
-      o2 += sw[c + 2] * part_o[((rb + c + 2) * n_q + h) * hd + d];
-      o3 += sw[c + 3] * part_o[((rb + c + 3) * n_q + h) * hd + d];
+      o0 += sw[c] * part_o[((rb + RG_SLOT(c)) * n_q + h) * hd + d];
+      o1 += sw[c + 1] * part_o[((rb + RG_SLOT(c + 1)) * n_q + h) * hd + d];
+      o2 += sw[c + 2] * part_o[((rb + RG_SLOT(c + 2)) * n_q + h) * hd + d];
+      o3 += sw[c + 3] * part_o[((rb + RG_SLOT(c + 3)) * n_q + h) * hd + d];
     }
-    for (; c < nc; ++c) o0 += sw[c] * part_o[((rb + c) * n_q + h) * hd + d];
+    for (; c < nc; ++c) o0 += sw[c] * part_o[((rb + RG_SLOT(c)) * n_q + h) * hd + d];
     act_store<SPLIT>(out, ((int64_t)r * n_q + h) * hd + d, ((o0 + o1) + (o2 + o3)) * invL);
   }
+#undef RG_SLOT
 }
 
 }  // namespace
 
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool,
                             KvGeom g, int layer, const int32_t* page_tab, int tab_stride,
-                            const int32_t* row_tab, const int32_t* row_pos, int max_ctx, int n_chunks,
-                            float* part_o, float* part_ml, const int* d_rows, int rows_ub, hipStream_t st) {
-  if (n_chunks < 1 || n_chunks > ATT_MAX_MERGE ||
+                            const int32_t* row_tab, const int32_t* row_pos, const int32_t* row_beg, int max_ctx,
+                            AttPlan plan, float* part_o, float* part_ml, const int* d_rows, int rows_ub,
+                            hipStream_t st) {
+  const int n_chunks = plan.n_chunks;
+  if (n_chunks < 1 || plan.n_slots != plan.pre_slots + n_chunks || plan.n_slots > ATT_MAX_MERGE ||
       std::max(128, (max_ctx + n_chunks - 1) / n_chunks + 31) > 16 * ATT_MAX_CHUNK_PAGES)
     return hipErrorInvalidValue;
   if (rows_ub <= 0) return hipSuccess;
@@ -404,7 +616,7 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
     hipLaunchKernelGGL(k_attention_mfma<HD>, grid1, dim3(64), 0, st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
-                       page_tab, tab_stride, row_tab, row_pos, n_chunks, rows_ub, part_o, part_ml, d_rows)
+                       page_tab, tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, d_rows)
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;
@@ -413,23 +625,51 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
 #undef RG_ATT_MFMA
   } else
     hipLaunchKernelGGL(k_attention<float>, grid, dim3(256), 0, st, q, n_q, n_kv, head_dim, (const float*)kv_pool,
-                       g, layer, page_tab, tab_stride, row_tab, row_pos, n_chunks, part_o, part_ml, d_rows);
+                       g, layer, page_tab, tab_stride, row_tab, row_pos, row_beg, plan, part_o, part_ml, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_prefix(const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool, KvGeom g,
+                                   int layer, const int32_t* page_tab, int tab_stride, int tab_base,
+                                   const int32_t* plen, const int32_t* grp_row0, const int32_t* grp_row1, int P,
+                                   int max_group_rows, AttPlan plan, float* part_o, float* part_ml, hipStream_t st) {
+  if (plan.pre_slots <= 0) return hipSuccess;
+  const int tiles = (max_group_rows * (n_q / n_kv) + 15) / 16;   // 16-row query tiles of the largest group
+  if (g.page_tok != 16 || plan.pre_chunk <= 0 || plan.pre_chunk % 32 || plan.pre_chunk > 1024 || tiles < 1 ||
+      P < 1)
+    return hipErrorInvalidValue;
+  const int n_rblk = (tiles + ATT_PRE_MAX_WAVES - 1) / ATT_PRE_MAX_WAVES;
+  const int waves = std::max(4, (tiles + n_rblk - 1) / n_rblk);
+  if ((int64_t)P * n_rblk > 65535) return hipErrorInvalidValue;
+  dim3 grid(plan.pre_slots, n_kv, P * n_rblk);
+  const bf16_t* pool = (const bf16_t*)kv_pool;
+  switch (head_dim) {
+    case 64:
+      hipLaunchKernelGGL(k_attention_prefix<64>, grid, dim3(64 * waves), 0, st, q, n_q, n_kv, pool, g, layer, page_tab,
+                         tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
+      break;
+    case 128:
+      hipLaunchKernelGGL(k_attention_prefix<128>, grid, dim3(64 * waves), 0, st, q, n_q, n_kv, pool, g, layer, page_tab,
+                         tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
+      break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_ml, int n_q, int head_dim,
-                             const int32_t* row_pos, int n_chunks, void* out, int64_t a_plane,
+                             const int32_t* row_pos, const int32_t* row_beg, AttPlan plan, void* out, int64_t a_plane,
                              const int* d_rows, int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
-  if (n_chunks < 1 || n_chunks > ATT_MAX_MERGE) return hipErrorInvalidValue;
+  if (plan.n_chunks < 1 || plan.n_slots > ATT_MAX_MERGE) return hipErrorInvalidValue;
   dim3 grid(rows_ub, n_q);
   int threads = head_dim >= 64 ? 64 * ((head_dim + 63) / 64) : 64;
   const ActOut o{out, a_plane};
   if (dtype == 1)
-    hipLaunchKernelGGL(k_attn_merge<1>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos,
-                       n_chunks, o, d_rows);
+    hipLaunchKernelGGL(k_attn_merge<1>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos, row_beg,
+                       plan, o, d_rows);
   else
-    hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos,
-                       n_chunks, o, d_rows);
+    hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos, row_beg,
+                       plan, o, d_rows);
   return hipGetLastError();
 }

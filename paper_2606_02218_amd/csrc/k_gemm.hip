@@ -361,7 +361,10 @@ int gemm_tile_rows(int dtype, int rows_ub) {
   return 256;
 }
 
-int gemm_tile_cols(int dtype, int rows_ub) { return 128; }
+// Prefill-sized row counts: 256 x 256 tiles of 64 x 128 per wave (twice the
+// MFMA work per LDS fragment; one wave per SIMD, which only pays with many
+// row blocks).
+int gemm_tile_cols(int dtype, int rows_ub) { return (dtype == 1 && rows_ub > 1024) ? 256 : 128; }
 
 hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
                        int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
@@ -378,7 +381,7 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
       case 32: e = launch_tiled<32, 128, 1, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 64: e = launch_tiled<64, 128, 2, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 128: e = launch_tiled<128, 128, 4, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
-      default: e = launch_tiled<256, 128, 4, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      default: e = launch_tiled<256, 256, 4, 8>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
     }
     if (e != hipSuccess || splits == 1) return e;
     return launch_split_epilogue<1, bf16_t>(d_rows, rows_ub, N, splits, ep, st);

@@ -22,22 +22,25 @@ __global__ void k_embed(const T* __restrict__ embed, int d, int V, const int32_t
 template <typename T>
 __global__ void k_decode_rows(const T* __restrict__ embed, int d, const int32_t* __restrict__ act_seq,
                               const int32_t* __restrict__ act_tok, const int32_t* __restrict__ seq_grp,
-                              const int32_t* __restrict__ plen, const int* __restrict__ d_t,
-                              int32_t* __restrict__ row_tab,
-                              int32_t* __restrict__ row_pos, float* __restrict__ x, const int* __restrict__ d_rows) {
+                              const int32_t* __restrict__ plen, const int* __restrict__ d_t, int prefix_split,
+                              int32_t* __restrict__ row_tab, int32_t* __restrict__ row_pos,
+                              int32_t* __restrict__ row_beg, float* __restrict__ x, const int* __restrict__ d_rows) {
   const int r = blockIdx.x;
   if (r >= *d_rows) return;
   const int s = act_seq[r];
   if (threadIdx.x == 0) {
+    const int L = plen[seq_grp[s]];
     row_tab[r] = s;
-    row_pos[r] = plen[seq_grp[s]] + *d_t - 1;
+    row_pos[r] = L + *d_t - 1;
+    row_beg[r] = prefix_split ? (L >> 4) << 4 : 0;
   }
   const T* e = embed + (int64_t)act_tok[r] * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ld_f32<T>(e + i);
 }
 
 __global__ void k_prefill_rows(const int32_t* __restrict__ prompt_off, int P, int tab_base,
-                               int32_t* __restrict__ row_tab, int32_t* __restrict__ row_pos, int total) {
+                               int32_t* __restrict__ row_tab, int32_t* __restrict__ row_pos,
+                               int32_t* __restrict__ row_beg, int total) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= total) return;
   int lo = 0, hi = P - 1;   // last p with prompt_off[p] <= r
@@ -47,6 +50,7 @@ __global__ void k_prefill_rows(const int32_t* __restrict__ prompt_off, int P, in
   }
   row_tab[r] = tab_base + lo;
   row_pos[r] = r - prompt_off[lo];
+  row_beg[r] = 0;
 }
 
 template <int SPLIT>
@@ -132,24 +136,24 @@ hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_
 }
 
 hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq, const int32_t* act_tok,
-                              const int32_t* seq_grp, const int32_t* plen, const int* d_t, int32_t* row_tab,
-                              int32_t* row_pos,
-                              float* x, const int* d_rows, int rows_ub, hipStream_t st) {
+                              const int32_t* seq_grp, const int32_t* plen, const int* d_t, int prefix_split,
+                              int32_t* row_tab, int32_t* row_pos, int32_t* row_beg, float* x, const int* d_rows,
+                              int rows_ub, hipStream_t st) {
   if (rows_ub <= 0) return hipSuccess;
   if (dtype == 1)
     hipLaunchKernelGGL(k_decode_rows<bf16_t>, dim3(rows_ub), dim3(256), 0, st, (const bf16_t*)embed, d, act_seq, act_tok,
-                       seq_grp, plen, d_t, row_tab, row_pos, x, d_rows);
+                       seq_grp, plen, d_t, prefix_split, row_tab, row_pos, row_beg, x, d_rows);
   else
     hipLaunchKernelGGL(k_decode_rows<float>, dim3(rows_ub), dim3(256), 0, st, (const float*)embed, d, act_seq, act_tok,
-                       seq_grp, plen, d_t, row_tab, row_pos, x, d_rows);
+                       seq_grp, plen, d_t, prefix_split, row_tab, row_pos, row_beg, x, d_rows);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_rows(const int32_t* prompt_off, int P, int tab_base, int32_t* row_tab, int32_t* row_pos,
-                               int total, hipStream_t st) {
+                               int32_t* row_beg, int total, hipStream_t st) {
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_prefill_rows, dim3((total + 255) / 256), dim3(256), 0, st, prompt_off, P, tab_base, row_tab,
-                     row_pos, total);
+                     row_pos, row_beg, total);
   return hipGetLastError();
 }
 

@@ -204,6 +204,16 @@ __global__ __launch_bounds__(1024) void k_compact(CompactArgs a) {
     ncarry += ntot;
   }
   if (ncarry > top) oom = true;
+  // pass 3: row range of every prompt among the kept rows (in sequence
+  // order, so each prompt's rows are contiguous)
+  const int M2 = oom ? 0 : kcarry;
+  for (int p = tid; p < a.P; p += blockDim.x) { a.grp_row0[p] = 0; a.grp_row1[p] = 0; }
+  __syncthreads();   // the resets and the compacted act_seq precede the range writes
+  for (int r = tid; r < M2; r += blockDim.x) {
+    const int p = a.seq_grp[a.act_seq[r]];
+    if (r == 0 || a.seq_grp[a.act_seq[r - 1]] != p) a.grp_row0[p] = r;
+    if (r == M2 - 1 || a.seq_grp[a.act_seq[r + 1]] != p) a.grp_row1[p] = r + 1;
+  }
   if (tid == 0) {
     if (t < a.hist_cap) {
       a.hist_active[t] = M;

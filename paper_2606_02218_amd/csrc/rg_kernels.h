@@ -60,37 +60,58 @@ hipError_t launch_embed(int dtype, const void* embed, int d, int V, const int32_
 
 // Decode row setup for step t = *d_t >= 1: row r (< *d_rows) feeds act_tok[r]
 // for sequence s = act_seq[r] at position plen[grp[s]] + t - 1; writes
-// row_tab, row_pos and the embedded token into x.
+// row_tab, row_pos, row_beg (the prompt's full-page length when
+// prefix_split, else 0) and the embedded token into x.
 hipError_t launch_decode_rows(int dtype, const void* embed, int d, const int32_t* act_seq,
                               const int32_t* act_tok, const int32_t* seq_grp, const int32_t* plen, const int* d_t,
-                              int32_t* row_tab, int32_t* row_pos, float* x, const int* d_rows,
-                              int rows_ub, hipStream_t st);
+                              int prefix_split, int32_t* row_tab, int32_t* row_pos, int32_t* row_beg, float* x,
+                              const int* d_rows, int rows_ub, hipStream_t st);
 
 // Prefill row setup: row r belongs to prompt p with prompt_off[p] <= r <
-// prompt_off[p+1]; row_tab[r] = tab_base + p, row_pos[r] = r - prompt_off[p].
+// prompt_off[p+1]; row_tab[r] = tab_base + p, row_pos[r] = r - prompt_off[p],
+// row_beg[r] = 0.
 hipError_t launch_prefill_rows(const int32_t* prompt_off, int P, int tab_base, int32_t* row_tab,
-                               int32_t* row_pos, int total, hipStream_t st);
+                               int32_t* row_pos, int32_t* row_beg, int total, hipStream_t st);
 
 // out[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g as an activation operand.  If
 // src_rows != NULL the input row is x[src_rows[r]].
 hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, float eps, void* out, int64_t a_plane,
                           const int32_t* src_rows, const int* d_rows, int rows_ub, hipStream_t st);
 
-// Paged causal attention.  Row r's context is positions 0..row_pos[r] of page
-// table row_tab[r] (at most max_ctx tokens); each row cuts its own context
-// into n_chunks equal chunks (rounded up to 32 tokens); each (row, kv head,
-// chunk) work item writes a partial (max, sum, unnormalised output) per query
-// head.
+// Partial slots of the attention of one row: slots 0..pre_slots-1 take the
+// shared-prefix chunks of pre_chunk tokens (prefix pass), slots
+// pre_slots..n_slots-1 the row's own n_chunks chunks (per-row pass).
+struct AttPlan {
+  int n_chunks;    // per-row chunks
+  int pre_slots;   // prefix chunks (0: no prefix pass)
+  int pre_chunk;   // tokens per prefix chunk, a multiple of 32
+  int n_slots;     // pre_slots + n_chunks
+};
+
+// Per-row pass.  Row r covers positions row_beg[r]..row_pos[r] of page table
+// row_tab[r] (at most max_ctx tokens), cut into n_chunks equal chunks
+// (rounded up to 32 tokens); each (row, kv head, chunk) work item writes a
+// partial (max, sum, unnormalised output) per query head.  row_beg[r] is a
+// multiple of 16.
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim,
                             const void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
-                            int tab_stride, const int32_t* row_tab, const int32_t* row_pos, int max_ctx,
-                            int n_chunks, float* part_o, float* part_ml, const int* d_rows,
+                            int tab_stride, const int32_t* row_tab, const int32_t* row_pos, const int32_t* row_beg,
+                            int max_ctx, AttPlan plan, float* part_o, float* part_ml, const int* d_rows,
                             int rows_ub, hipStream_t st);
 
-// Merge the chunk partials of each (row, q head) into the activation operand
+// Prefix pass (bf16 models).  The active rows of prompt p are grp_row0[p] ..
+// grp_row1[p]-1 (empty when equal); all of them attend to positions
+// 0..(plen[p]/16)*16-1 of page table row tab_base + p, which every row of the
+// group has as its row_beg.  max_group_rows bounds grp_row1[p] - grp_row0[p].
+hipError_t launch_attention_prefix(const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool, KvGeom g,
+                                   int layer, const int32_t* page_tab, int tab_stride, int tab_base,
+                                   const int32_t* plen, const int32_t* grp_row0, const int32_t* grp_row1, int P,
+                                   int max_group_rows, AttPlan plan, float* part_o, float* part_ml, hipStream_t st);
+
+// Merge the partial slots of each (row, q head) into the activation operand
 // out [rows][n_q*head_dim].
 hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_ml, int n_q,
-                             int head_dim, const int32_t* row_pos, int n_chunks, void* out,
+                             int head_dim, const int32_t* row_pos, const int32_t* row_beg, AttPlan plan, void* out,
                              int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
 
 // x[r][n] += sum_s C[s][r][n] (C may be NULL: no add; one block per 256
@@ -123,8 +144,11 @@ struct SampleArgs {
 hipError_t launch_sample(const SampleArgs& a, int rows_ub, hipStream_t st);
 
 // Retire/compact after the step whose index is state[8]; advances state[8].
+// Also publishes each prompt's range of rows among the surviving ones
+// (grp_row0[p] .. grp_row1[p]-1; compaction keeps rows in sequence order).
 struct CompactArgs {
-  int max_new, page_tok, max_pages, n_seq;
+  int max_new, page_tok, max_pages, n_seq, P;
+  int32_t* grp_row0; int32_t* grp_row1;
   int32_t* act_seq; int32_t* act_tok; const int32_t* done;
   const int32_t* seq_grp; const int32_t* plen;
   int32_t* page_tab; int32_t* seq_npages; const int32_t* seq_nshared;

@@ -8,6 +8,9 @@
   (6 query heads per kv head, head_dim 128), and a gpt2s-shaped bf16 decoder
   with ragged prompt lengths (partial KV pages) and variable G.
 * shared prompt pages give bit-identical results to per-sibling copies.
+* the group prefix pass (each prompt's full prefix pages attended once per
+  group) agrees with the row-by-row pass within rounding and with the oracle,
+  also for a group larger than one prefix workgroup's 128 query rows.
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -46,14 +49,14 @@ def _case(shape, seed, plens, G, max_new, len_range):
     return prompts, L
 
 
-def _run_tf(torch, shape, w, prompts, G, max_new, L, seed, share=True):
+def _run_tf(torch, shape, w, prompts, G, max_new, L, seed, share=True, group_prefix=False):
     model = oracle_for(shape, w)
     ref = oracle_rollout(model, prompts, G, max_new, seed, L, record_steps=max_new)
     pol = make_policy(shape, w, max_seqs=int(np.sum(G)), max_prompts=len(G), max_prompt_tokens=int(sum(map(len, prompts))),
                       max_context=max(map(len, prompts)) + max_new)
     ft = torch.from_numpy(ref["tokens"]).cuda()
     tok, ln, lp, dump = pol.rollout(prompts_to_device(prompts), G, max_new, seed, forced_len=L, force_tokens=ft,
-                                    dump_steps=max_new, share_prefix=share)
+                                    dump_steps=max_new, share_prefix=share, group_prefix_pass=group_prefix)
     torch.cuda.synchronize()
     return ref, _np(tok), _np(ln), _np(lp), _np(dump), pol
 
@@ -124,11 +127,29 @@ def test_gpt2s_ragged_teacher_forced_and_sharing(torch):
     np.testing.assert_array_equal(_np(ln2), ln)
     np.testing.assert_array_equal(_np(lp2), lp)
     np.testing.assert_array_equal(_np(dump2), dump)
+    # attending to the prefix once per group changes only the summation order
+    tok4, ln4, lp4, dump4 = pol.rollout(prompts_to_device(prompts), G, 40, 1234, forced_len=L, force_tokens=ft,
+                                        dump_steps=40, group_prefix_pass=True)
+    _check_tf(ref, _np(tok4), _np(ln4), _np(lp4), _np(dump4), L)
+    live = np.zeros(dump.shape[:2], dtype=bool)
+    for s in range(len(L)):
+        live[: int(L[s]), s] = True
+    assert float(np.max(np.abs(_np(dump4)[live] - dump[live]))) < 2e-3
     # free-running from the same inputs follows the oracle's trajectory
     tok3, ln3, lp3 = pol.rollout(prompts_to_device(prompts), G, 40, 1234, forced_len=L)
     tok3, ln3, lp3 = _np(tok3), _np(ln3), _np(lp3)
     check_structure(tok3, ln3, lp3, GPT2S.eos_id, 40, L)
     compare_free_running(tok3, lp3, ref, ln3, lp_tol=2 * LOGIT_TOL)
+
+
+def test_gqa_bf16_large_group(torch):
+    # 30 siblings x 6 query heads per kv head = 180 query rows: two prefix
+    # workgroups per (prompt, kv head, chunk); the second group retires early
+    w = make_weights(GQA, 5)
+    prompts, L = _case(GQA, 5, [70, 33], [30, 2], 12, (1, 12))
+    L[30:] = [2, 3]
+    ref, tok, ln, lp, dump, _ = _run_tf(torch, GQA, w, prompts, [30, 2], 12, L, 21, group_prefix=True)
+    _check_tf(ref, tok, ln, lp, dump, L)
 
 
 def test_natural_eos(torch):
