@@ -138,6 +138,20 @@ struct rg_policy {
   }
 };
 
+// ---------------------------------------------------------------- launch-event hook
+namespace {
+thread_local hipEvent_t g_arm_start = nullptr, g_arm_stop = nullptr;
+}
+void rg_arm_launch_events(hipEvent_t start, hipEvent_t stop) { g_arm_start = start; g_arm_stop = stop; }
+bool rg_take_launch_events(hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_arm_start) return false;
+  *start = g_arm_start;
+  *stop = g_arm_stop;
+  g_arm_start = g_arm_stop = nullptr;
+  return true;
+}
+bool rg_launch_events_armed() { return g_arm_start != nullptr; }
+
 namespace {
 
 // ---------------------------------------------------------------- profiling
@@ -152,33 +166,51 @@ int prof_drain_one(rg_policy* p) {
   return RG_OK;
 }
 
+// Times one launcher call of a kernel class.  Bracketing: events recorded on
+// the stream before and after the call (every class; includes the stream's
+// dispatch overhead).  Dispatch (ext = true, single-kernel launchers that
+// take armed events): the events are the kernel dispatch's own timestamps.
 struct ProfScope {
   rg_policy* p;
   hipStream_t st;
   int64_t slot = -1;
+  bool ext = false;
   int rc = RG_OK;
-  ProfScope(rg_policy* pol, hipStream_t s, int kind) : p(pol), st(s) {
+  ProfScope(rg_policy* pol, hipStream_t s, int kind, bool dispatch_events) : p(pol), st(s) {
     if (!p->prof || !((p->prof_mask >> kind) & 1u)) return;
     if (p->prof_head - p->prof_tail >= RG_PROF_RING) rc = prof_drain_one(p);
     slot = p->prof_head % RG_PROF_RING;
     p->prof_kind[slot] = kind;
     p->prof_ph[slot] = p->prof_phase;
-    (void)hipEventRecord(p->prof_ev[2 * slot], st);
+    ext = dispatch_events;
+    if (ext) rg_arm_launch_events(p->prof_ev[2 * slot], p->prof_ev[2 * slot + 1]);
+    else (void)hipEventRecord(p->prof_ev[2 * slot], st);
   }
   ~ProfScope() {
     if (slot < 0) return;
-    (void)hipEventRecord(p->prof_ev[2 * slot + 1], st);
+    if (ext) {
+      if (rg_launch_events_armed()) {   // the launcher launched nothing
+        hipEvent_t a, b;
+        rg_take_launch_events(&a, &b);
+        return;
+      }
+    } else {
+      (void)hipEventRecord(p->prof_ev[2 * slot + 1], st);
+    }
     p->prof_head++;
   }
 };
 
-#define LAUNCH(kind, call)                                                                    \
+#define LAUNCH_(kind, call, ext)                                                              \
   do {                                                                                        \
-    ProfScope ps_(pol, st, kind);                                                             \
+    ProfScope ps_(pol, st, kind, ext);                                                        \
     if (ps_.rc != RG_OK) return ps_.rc;                                                        \
     hipError_t e_ = (call);                                                                   \
     if (e_ != hipSuccess) return fail(RG_EHIP, std::string("launch ") + #kind + ": " + hipGetErrorString(e_)); \
   } while (0)
+#define LAUNCH(kind, call) LAUNCH_(kind, call, false)
+// single-kernel launchers that time their dispatch with armed events
+#define LAUNCH_TIMED(kind, call) LAUNCH_(kind, call, true)
 
 // Split-K factor of a projection: enough blocks to cover the chip, each
 // split at least two 64-wide K steps, and the fp32 split partials (written
@@ -284,11 +316,11 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     if ((rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, d_rows, rows_ub, qkv)))
       return rc;
     if (plan.pre_slots)
-      LAUNCH(RG_K_ATTN, launch_attention_prefix(pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
+      LAUNCH_TIMED(RG_K_ATTN, launch_attention_prefix(pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                                 pol->page_tab, tab_stride, pre->tab_base, pol->plen,
                                                 pol->grp_row0, pol->grp_row1, pre->P, pre->max_group_rows, plan,
                                                 pol->att_o, pol->att_ml, st));
-    LAUNCH(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
+    LAUNCH_TIMED(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                        pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, pol->row_beg, ctx_max,
                                        plan, pol->att_o, pol->att_ml, d_rows, rows_ub, st));
     LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,

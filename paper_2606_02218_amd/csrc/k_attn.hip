@@ -1,8 +1,8 @@
 // Paged causal attention over the KV pool, for prefill rows and decode rows
 // alike.  Row r attends to positions 0..row_pos[r] through page table
 // row_tab[r]; position j lives in page page_tab[tab*tab_stride + j/16], slot
-// j % 16.  Inside a page a layer holds K as [kv head][slot][dim] and V
-// transposed, [kv head][dim][slot].  Every work item keeps a running softmax
+// j % 16, in the key and value slabs of kv_k_off / kv_v_off (16-byte granules
+// of 8 dims of a token, resp. 8 tokens of a dim).  Every work item keeps a running softmax
 // (max, sum) and an unnormalised output per query head of its GQA group in a
 // partial slot of the row; the merge kernel combines a row's slots.
 //
@@ -28,6 +28,7 @@
 
 #include "rg_device.h"
 #include "rg_kernels.h"
+#include <hip/hip_ext.h>
 
 namespace {
 
@@ -88,8 +89,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     sq[i] = q[((int64_t)r * n_q + kvh * rep) * hd + i];
   if (tid < rep) { s_m[tid] = -INFINITY; s_l[tid] = 0.f; }
   const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * g.page_tok * hd;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * g.page_tok * hd;   // V^T [dim][slot]
+  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * hd;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * hd;
 
   // each thread owns output slots (h, d) = idx / hd, idx % hd for idx = tid + 256*k
   const int n_own = (rep * hd + 255) / 256;
@@ -103,13 +104,13 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     // ---- scores: one token per thread
     if (tid < nt) {
       const int j = t0 + tid;
-      const KV* kp = pool + (int64_t)tab[j / g.page_tok] * g.page_elems + koff + (int64_t)(j % g.page_tok) * hd;
+      const KV* kp = pool + (int64_t)tab[j >> 4] * g.page_elems + koff;
       float dot[ATT_MAX_REP];
 #pragma unroll
       for (int h = 0; h < ATT_MAX_REP; ++h) dot[h] = 0.f;
       for (int d = 0; d < hd; d += 8) {
         float kv8[8];
-        load8_f32<KV>(kp + d, kv8);
+        load8_f32<KV>(kp + kv_k_off(j & 15, d), kv8);   // dims d .. d+7 of token j
 #pragma unroll
         for (int h = 0; h < ATT_MAX_REP; ++h) {
           if (h < rep) {
@@ -147,8 +148,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
         float a = acc[k] * s_alpha[h];
         for (int jj = 0; jj < nt; ++jj) {
           const int j = t0 + jj;
-          const KV* vp = pool + (int64_t)tab[j / g.page_tok] * g.page_elems + voff + (int64_t)d * g.page_tok;
-          a = fmaf(sp[h * ATT_TILE + jj], ld_f32<KV>(vp + (j % g.page_tok)), a);
+          const KV* vp = pool + (int64_t)tab[j >> 4] * g.page_elems + voff;
+          a = fmaf(sp[h * ATT_TILE + jj], ld_f32<KV>(vp + kv_v_off(j & 15, d, hd)), a);
         }
         acc[k] = a;
       }
@@ -325,8 +326,10 @@ struct AttBlock {
 
 // K: A-fragment row i of tile tt is token t0 + 8*(i/4) + 4*tt + (i%4), so that
 // the S^T layout leaves lane group grp holding tokens t0+8*grp .. +7; the
-// lane's two rows share one page.  V^T: dims dt*16 + col, tokens t0+8*grp ..
-// +7 (one page slot run).  Tokens past c1 read token c0 instead (masked).
+// lane's two rows share one page, and lanes 4q..4q+3 read 4 neighbouring
+// tokens (64 contiguous bytes of a key slab).  V^T: dims dt*16 + col, tokens
+// t0+8*grp .. +7 (one granule).  Tokens past c1 read token c0 instead
+// (masked).  t0 is a multiple of 16.
 template <int HD>
 __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restrict__ pool, const KvGeom& g,
                                          int64_t koff, int64_t voff, const int* spg, int c0, int c1, int t0,
@@ -335,15 +338,15 @@ __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restri
   for (int tt = 0; tt < 2; ++tt) {
     int tok = t0 + 8 * (col >> 2) + 4 * tt + (col & 3);
     if (tok >= c1) tok = c0;
-    const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff + (int64_t)(tok & 15) * HD + 8 * grp;
+    const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff + kv_k_off(tok & 15, 8 * grp);
 #pragma unroll
-    for (int kb = 0; kb < HD / 32; ++kb) b.k[tt][kb] = *reinterpret_cast<const u32x4_t*>(kp + kb * 32);
+    for (int kb = 0; kb < HD / 32; ++kb) b.k[tt][kb] = *reinterpret_cast<const u32x4_t*>(kp + kb * 4 * 128);
   }
   const int tv = t0 + 8 * grp;
   const int pg = spg[((tv < c1 ? tv : c0) - c0) >> 4];
-  const bf16_t* vp = pool + (int64_t)pg * g.page_elems + voff + (tv & 15);
+  const bf16_t* vp = pool + (int64_t)pg * g.page_elems + voff + kv_v_off(tv & 15, col, HD);
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) b.v[dt] = *reinterpret_cast<const u32x4_t*>(vp + (int64_t)(dt * 16 + col) * 16);
+  for (int dt = 0; dt < HD / 16; ++dt) b.v[dt] = *reinterpret_cast<const u32x4_t*>(vp + dt * 16 * 8);
 }
 
 template <int HD>
@@ -496,18 +499,18 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
     for (int k = 0; k < MAXP; ++k) {
       const int pc = tid + k * nthr;
       if (pc < PIECES) {
-        if (pc < 4 * HD) {                       // K: token tk, 8 dims from ck*8
-          const int tk = pc / (HD / 8), ck = pc % (HD / 8);
+        if (pc < 4 * HD) {                       // K: token tk, 8 dims from ck*8 (neighbouring threads: tokens)
+          const int tk = pc & 31, ck = pc >> 5;
           int tok = t0 + tk;
           if (tok >= c1) tok = c0;
           rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff +
-                                                    (int64_t)(tok & 15) * HD + ck * 8);
-        } else {                                 // V^T: dim dd, tokens q4*8 .. +7
-          const int pv = pc - 4 * HD, dd = pv >> 2, q4 = pv & 3;
+                                                    kv_k_off(tok & 15, ck * 8));
+        } else {                                 // V^T: dim dd, tokens q4*8 .. +7 (neighbouring threads: dims)
+          const int pv = pc - 4 * HD, dd = pv % HD, q4 = pv / HD;
           int tv = t0 + q4 * 8;
           if (tv >= c1) tv = c0;
           rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tv - c0) >> 4] * g.page_elems + voff +
-                                                    (int64_t)dd * 16 + (tv & 15));
+                                                    kv_v_off(tv & 15, dd, HD));
         }
       }
     }
@@ -518,11 +521,11 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
       const int pc = tid + k * nthr;
       if (pc < PIECES) {
         if (pc < 4 * HD) {
-          const int tk = pc / (HD / 8), ck = pc % (HD / 8);
+          const int tk = pc & 31, ck = pc >> 5;
           const int lrow = 16 * ((tk >> 2) & 1) + (((tk >> 3) << 2) | (tk & 3));   // fragment lane order
           *reinterpret_cast<u32x4_t*>(&sK[buf][lrow * KROW + ck * 8]) = rg[k];
         } else {
-          const int pv = pc - 4 * HD, dd = pv >> 2, q4 = pv & 3;
+          const int pv = pc - 4 * HD, dd = pv % HD, q4 = pv / HD;
           *reinterpret_cast<u32x4_t*>(&sV[buf][dd * VROW + q4 * 8]) = rg[k];
         }
       }
@@ -598,6 +601,16 @@ __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __re
 
 }  // namespace
 
+// One kernel launch; with armed timing events they time the dispatch itself.
+template <typename F, typename... Args>
+void att_launch(F kernel, dim3 grid, dim3 block, hipStream_t st, Args... args) {
+  hipEvent_t e0, e1;
+  if (rg_take_launch_events(&e0, &e1))
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+}
+
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool,
                             KvGeom g, int layer, const int32_t* page_tab, int tab_stride,
                             const int32_t* row_tab, const int32_t* row_pos, const int32_t* row_beg, int max_ctx,
@@ -615,8 +628,8 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
-    hipLaunchKernelGGL(k_attention_mfma<HD>, grid1, dim3(64), 0, st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
-                       page_tab, tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, d_rows)
+    att_launch(k_attention_mfma<HD>, grid1, dim3(64), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, page_tab, \
+               tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, d_rows)
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;
@@ -624,8 +637,8 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     }
 #undef RG_ATT_MFMA
   } else
-    hipLaunchKernelGGL(k_attention<float>, grid, dim3(256), 0, st, q, n_q, n_kv, head_dim, (const float*)kv_pool,
-                       g, layer, page_tab, tab_stride, row_tab, row_pos, row_beg, plan, part_o, part_ml, d_rows);
+    att_launch(k_attention<float>, grid, dim3(256), st, q, n_q, n_kv, head_dim, (const float*)kv_pool, g, layer,
+               page_tab, tab_stride, row_tab, row_pos, row_beg, plan, part_o, part_ml, d_rows);
   return hipGetLastError();
 }
 
@@ -645,12 +658,12 @@ hipError_t launch_attention_prefix(const float* q, int n_q, int n_kv, int head_d
   const bf16_t* pool = (const bf16_t*)kv_pool;
   switch (head_dim) {
     case 64:
-      hipLaunchKernelGGL(k_attention_prefix<64>, grid, dim3(64 * waves), 0, st, q, n_q, n_kv, pool, g, layer, page_tab,
-                         tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
+      att_launch(k_attention_prefix<64>, grid, dim3(64 * waves), st, q, n_q, n_kv, pool, g, layer, page_tab,
+                 tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
       break;
     case 128:
-      hipLaunchKernelGGL(k_attention_prefix<128>, grid, dim3(64 * waves), 0, st, q, n_q, n_kv, pool, g, layer, page_tab,
-                         tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
+      att_launch(k_attention_prefix<128>, grid, dim3(64 * waves), st, q, n_q, n_kv, pool, g, layer, page_tab,
+                 tab_stride, tab_base, plen, grp_row0, grp_row1, n_rblk, plan, part_o, part_ml);
       break;
     default: return hipErrorInvalidValue;
   }

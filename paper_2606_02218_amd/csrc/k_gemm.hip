@@ -71,11 +71,11 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float
   KV* pool = (KV*)ep.kv_pool;
   if (head >= ep.n_q + ep.n_kv) {                     // value head: no rotation, V^T layout
     const int kvh = head - ep.n_q - ep.n_kv;
-    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / ep.geom.page_tok];
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
     KV* vb = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
-             ((int64_t)ep.n_kv + kvh) * ep.geom.page_tok * hd + pos % ep.geom.page_tok;
-    kv_store<KV>(vb + (int64_t)d * ep.geom.page_tok, a);
-    kv_store<KV>(vb + (int64_t)(d + half) * ep.geom.page_tok, b);
+             ((int64_t)ep.n_kv + kvh) * 16 * hd;
+    kv_store<KV>(vb + kv_v_off(pos & 15, d, hd), a);
+    kv_store<KV>(vb + kv_v_off(pos & 15, d + half, hd), b);
     return;
   }
   const float co = ep.rope_cos[(int64_t)pos * half + d], si = ep.rope_sin[(int64_t)pos * half + d];
@@ -86,11 +86,11 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float
     qo[d + half] = rb;
   } else {
     const int kvh = head - ep.n_q;
-    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / ep.geom.page_tok];
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
     KV* kp = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
-             ((int64_t)kvh * ep.geom.page_tok + pos % ep.geom.page_tok) * hd;
-    kv_store<KV>(kp + d, ra);
-    kv_store<KV>(kp + d + half, rb);
+             (int64_t)kvh * 16 * hd;
+    kv_store<KV>(kp + kv_k_off(pos & 15, d), ra);
+    kv_store<KV>(kp + kv_k_off(pos & 15, d + half), rb);
   }
 }
 
@@ -126,7 +126,7 @@ __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, i
   }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, int EPI>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
     const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep) {
@@ -151,28 +151,32 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int lr = lane & 15, lk = (lane >> 4) * 8;
 
-  u32x4_t ra[A_PER_T], rw[W_PER_T];
-#define RG_FETCH(KK)                                                                                          \
+  // STAGES register sets: the global loads of step k + STAGES*BK are issued
+  // right after step k's tiles reach LDS, so STAGES steps of loads are in
+  // flight while one step is multiplied out (HBM latency exceeds one step of
+  // MFMA work by a wide margin).
+  u32x4_t ra[STAGES][A_PER_T], rw[STAGES][W_PER_T];
+#define RG_FETCH(S, KK)                                                                                       \
   _Pragma("unroll") for (int i = 0; i < A_PER_T; ++i) {                                                       \
     const int p = tid + i * NT;                                                                               \
     const int plane = p / A_PIECES, q = p % A_PIECES;                                                         \
     const int row = min(m0 + q / (BK / 8), M - 1); /* rows past M are computed, never stored */              \
-    ra[i] = *reinterpret_cast<const u32x4_t*>(A + plane * a_plane + (int64_t)row * lda + (KK) + (q % (BK / 8)) * 8); \
+    ra[S][i] = *reinterpret_cast<const u32x4_t*>(A + plane * a_plane + (int64_t)row * lda + (KK) + (q % (BK / 8)) * 8); \
   }                                                                                                           \
   _Pragma("unroll") for (int i = 0; i < W_PER_T; ++i) {                                                       \
     const int p = tid + i * NT;                                                                               \
     const int col = min(n0 + p / (BK / 8), N - 1);                                                            \
-    rw[i] = *reinterpret_cast<const u32x4_t*>(W + (int64_t)col * ldw + (KK) + (p % (BK / 8)) * 8);           \
+    rw[S][i] = *reinterpret_cast<const u32x4_t*>(W + (int64_t)col * ldw + (KK) + (p % (BK / 8)) * 8);        \
   }
-#define RG_STASH()                                                                                            \
+#define RG_STASH(S)                                                                                           \
   _Pragma("unroll") for (int i = 0; i < A_PER_T; ++i) {                                                       \
     const int p = tid + i * NT;                                                                               \
     const int plane = p / A_PIECES, q = p % A_PIECES;                                                         \
-    *reinterpret_cast<u32x4_t*>(&sA[plane][(q / (BK / 8)) * LROW + (q % (BK / 8)) * 8]) = ra[i];             \
+    *reinterpret_cast<u32x4_t*>(&sA[plane][(q / (BK / 8)) * LROW + (q % (BK / 8)) * 8]) = ra[S][i];          \
   }                                                                                                           \
   _Pragma("unroll") for (int i = 0; i < W_PER_T; ++i) {                                                       \
     const int p = tid + i * NT;                                                                               \
-    *reinterpret_cast<u32x4_t*>(&sW[(p / (BK / 8)) * LROW + (p % (BK / 8)) * 8]) = rw[i];                    \
+    *reinterpret_cast<u32x4_t*>(&sW[(p / (BK / 8)) * LROW + (p % (BK / 8)) * 8]) = rw[S][i];                 \
   }
 
   f32x4_t acc[WM][WN];
@@ -181,27 +185,33 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (kb0 < ke) {
-    RG_FETCH(kb0)
-    for (int k = kb0; k < ke; k += BK) {
-      __syncthreads();          // the previous step's fragment reads are done
-      RG_STASH()
-      __syncthreads();
-      if (k + BK < ke) { RG_FETCH(k + BK) }   // next tiles in flight while this one is multiplied
 #pragma unroll
-      for (int ks = 0; ks < BK; ks += 32) {
-        bf16x8_t bw[WN];
+  for (int s = 0; s < STAGES; ++s)
+    if (kb0 + s * BK < ke) { RG_FETCH(s, kb0 + s * BK) }
+  for (int k = kb0; k < ke; k += STAGES * BK) {
 #pragma unroll
-        for (int j = 0; j < WN; ++j) bw[j] = lds_frag(&sW[((wn * WN + j) * 16 + lr) * LROW + ks + lk]);
+    for (int s = 0; s < STAGES; ++s) {
+      const int kk = k + s * BK;
+      if (kk < ke) {
+        __syncthreads();          // the previous step's fragment reads are done
+        RG_STASH(s)
+        __syncthreads();
+        if (kk + STAGES * BK < ke) { RG_FETCH(s, kk + STAGES * BK) }
 #pragma unroll
-        for (int i = 0; i < WM; ++i) {
-          const int arow = (wm * WM + i) * 16 + lr;
-          const bf16x8_t ah = lds_frag(&sA[0][arow * LROW + ks + lk]);
-          const bf16x8_t al = lds_frag(&sA[1][arow * LROW + ks + lk]);
+        for (int ks = 0; ks < BK; ks += 32) {
+          bf16x8_t bw[WN];
 #pragma unroll
-          for (int j = 0; j < WN; ++j) {
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[j], acc[i][j], 0, 0, 0);
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[j], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < WN; ++j) bw[j] = lds_frag(&sW[((wn * WN + j) * 16 + lr) * LROW + ks + lk]);
+#pragma unroll
+          for (int i = 0; i < WM; ++i) {
+            const int arow = (wm * WM + i) * 16 + lr;
+            const bf16x8_t ah = lds_frag(&sA[0][arow * LROW + ks + lk]);
+            const bf16x8_t al = lds_frag(&sA[1][arow * LROW + ks + lk]);
+#pragma unroll
+            for (int j = 0; j < WN; ++j) {
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[j], acc[i][j], 0, 0, 0);
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[j], acc[i][j], 0, 0, 0);
+            }
           }
         }
       }
@@ -310,13 +320,13 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
   C[(int64_t)r * N + n] = acc;
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int STAGES>
 hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
                         int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   constexpr int NT = (BM / (16 * WM)) * (BN / (16 * WN)) * 64;
   dim3 grid((N + BN - 1) / BN, (rows_ub + BM - 1) / BM, splits);
 #define RG_TILED(E)                                                                                           \
-  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, E>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane, \
+  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, E>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane, \
                      (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep)
   if (splits > 1) {
     RG_TILED(GEMM_EPI_PARTIAL);
@@ -377,11 +387,11 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
   if (dtype == 1) {
     if (K % BK || k_per_split % BK || N % 16) return hipErrorInvalidValue;
     switch (gemm_tile_rows(dtype, rows_ub)) {
-      case 16: e = launch_tiled<16, 128, 1, 2>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
-      case 32: e = launch_tiled<32, 128, 1, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
-      case 64: e = launch_tiled<64, 128, 2, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
-      case 128: e = launch_tiled<128, 128, 4, 4>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
-      default: e = launch_tiled<256, 256, 4, 8>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 16: e = launch_tiled<16, 128, 1, 2, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 32: e = launch_tiled<32, 128, 1, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 64: e = launch_tiled<64, 128, 2, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      case 128: e = launch_tiled<128, 128, 4, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
+      default: e = launch_tiled<256, 256, 4, 8, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
     }
     if (e != hipSuccess || splits == 1) return e;
     return launch_split_epilogue<1, bf16_t>(d_rows, rows_ub, N, splits, ep, st);

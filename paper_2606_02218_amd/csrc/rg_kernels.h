@@ -9,13 +9,33 @@
 #include "rg_device.h"
 
 struct KvGeom {
-  int page_tok;        // tokens per page
+  int page_tok;        // tokens per page (16)
   int n_layers, n_kv, head_dim;
   int64_t page_elems;  // elements of one page across all layers
   int64_t layer_elems; // elements of one layer inside a page: 2 * n_kv * page_tok * head_dim
-  // K of (layer l, kv head h, slot j, dim d) at  page*page_elems + l*layer_elems + (h*page_tok + j)*head_dim + d
-  // V (transposed) at  page*page_elems + l*layer_elems + n_kv*page_tok*head_dim + (h*head_dim + d)*page_tok + j
 };
+
+// Inside a page, layer l holds a key slab per kv head h at
+//   page*page_elems + l*layer_elems + h*16*head_dim
+// and a value slab at
+//   page*page_elems + l*layer_elems + (n_kv + h)*16*head_dim.
+// Both slabs are made of 16-byte granules of 8 elements (bf16): keys as
+// [d/8][slot][8] (8 consecutive dims of one token), values as [slot/8][d][8]
+// (8 consecutive tokens of one dim).  A quarter-wave of lanes reading the
+// same dims of 4 neighbouring tokens (keys) or the same tokens of 4
+// neighbouring dims (values) then touches 64 contiguous bytes.
+__host__ __device__ inline int64_t kv_k_off(int slot, int d) { return (int64_t)(d >> 3) * 128 + slot * 8 + (d & 7); }
+__host__ __device__ inline int64_t kv_v_off(int slot, int d, int hd) {
+  return (int64_t)(slot >> 3) * hd * 8 + (int64_t)d * 8 + (slot & 7);
+}
+
+// Kernel timing hook.  The profiler arms a (start, stop) event pair for the
+// next launch; a launcher that supports it takes the pair and launches its
+// kernel with hipExtLaunchKernelGGL, so that the events time the kernel's own
+// dispatch rather than the stream around it.
+void rg_arm_launch_events(hipEvent_t start, hipEvent_t stop);
+bool rg_take_launch_events(hipEvent_t* start, hipEvent_t* stop);   // disarms
+bool rg_launch_events_armed();
 
 // dtype: 0 = fp32 storage, 1 = bf16 storage.  Activation operands (`act`,
 // `a_plane`) follow ActOut in rg_device.h: fp32 for fp32 models, hi/lo bf16
