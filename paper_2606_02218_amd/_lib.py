@@ -1,4 +1,5 @@
-"""ctypes marshalling for include/rollout.h.  No computation happens here."""
+"""ctypes marshalling for include/rollout.h and include/sagc.h.  No computation
+happens here."""
 from __future__ import annotations
 
 import ctypes as C
@@ -18,7 +19,9 @@ KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge"
                 "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup"]
 
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
-           "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times"]
+           "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
+           "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw"]
+SAGC_MAX_SIZES = 8
 
 
 class RolloutError(RuntimeError):
@@ -53,6 +56,17 @@ class rg_sampling(C.Structure):
                 ("profile_kinds", C.c_uint32)]
 
 
+class sagc_config(C.Structure):
+    _fields_ = [("n_sizes", C.c_int32), ("sizes", C.c_int32 * SAGC_MAX_SIZES), ("tau", C.c_double),
+                ("delta", C.c_double), ("eta", C.c_double), ("gamma", C.c_double), ("seed", C.c_uint64)]
+
+
+class sagc_state(C.Structure):
+    _fields_ = [("lam", C.c_double), ("alpha", C.c_double * SAGC_MAX_SIZES), ("beta", C.c_double * SAGC_MAX_SIZES),
+                ("g_index", C.c_int32), ("reserved", C.c_int32), ("step", C.c_int64), ("last_rate", C.c_double),
+                ("last_sample", C.c_double * SAGC_MAX_SIZES), ("last_score", C.c_double * SAGC_MAX_SIZES)]
+
+
 def lib_path() -> str:
     return _LIB_PATH
 
@@ -82,6 +96,12 @@ def load_library():
     lib.rg_gumbel_bits.argtypes = [C.c_uint64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
     lib.rg_step_history.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rg_kernel_times.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    lib.sagc_init.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state)]
+    lib.sagc_group_stats.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p,
+                                     C.c_void_p]
+    lib.sagc_step.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state), C.POINTER(C.c_float), C.c_int32,
+                              C.POINTER(C.c_int32)]
+    lib.sagc_beta_draw.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_double, C.c_double, C.POINTER(C.c_double)]
     _lib = lib
     return lib
 
@@ -257,3 +277,63 @@ def gumbel_bits(seed: int, t: int, s: int, vocab: int, stream=None):
     out = torch.empty(vocab, dtype=torch.int32, device="cuda")
     _check(lib.rg_gumbel_bits(C.c_uint64(seed), t, s, vocab, _ptr(out), _stream_ptr(stream)))
     return out
+
+
+class Sagc:
+    """Straggler-aware group-size controller (include/sagc.h): host state,
+    one step per rollout."""
+
+    def __init__(self, sizes=(4, 8, 16), tau: float = 1.25, delta: float = 0.1, eta: float = 0.5,
+                 gamma: float = 0.95, seed: int = 0):
+        lib = load_library()
+        sizes = [int(s) for s in sizes]
+        if not 1 <= len(sizes) <= SAGC_MAX_SIZES:
+            raise ValueError("between 1 and 8 sizes")
+        arr = (C.c_int32 * SAGC_MAX_SIZES)(*(sizes + [0] * (SAGC_MAX_SIZES - len(sizes))))
+        self.cfg = sagc_config(len(sizes), arr, float(tau), float(delta), float(eta), float(gamma),
+                               C.c_uint64(seed & (2 ** 64 - 1)))
+        self.sizes = sizes
+        self.state = sagc_state()
+        _check(lib.sagc_init(C.byref(self.cfg), C.byref(self.state)))
+
+    @property
+    def G(self) -> int:
+        return self.sizes[self.state.g_index]
+
+    def group_stats(self, lengths, G_dev, out=None, stream=None):
+        """lengths: device int32 [N]; G_dev: device int32 [P].  Returns device
+        float [P, 4] = (l_max, l_median, R, S)."""
+        import torch
+        lib = load_library()
+        P = int(G_dev.numel())
+        if out is None:
+            out = torch.empty((P, 4), dtype=torch.float32, device=lengths.device)
+        _check(lib.sagc_group_stats(_ptr(lengths), _ptr(G_dev), P, int(lengths.numel()), self.cfg.tau, _ptr(out),
+                                    _stream_ptr(stream)))
+        return out
+
+    def step(self, stats) -> int:
+        """stats: [n_groups, 4] (host numpy or any tensor; column 3 = S).
+        Returns the next group size."""
+        lib = load_library()
+        if hasattr(stats, "detach"):
+            stats = stats.detach().cpu().numpy()
+        s = np.ascontiguousarray(np.asarray(stats, dtype=np.float32).reshape(-1, 4))
+        g = C.c_int32()
+        _check(lib.sagc_step(C.byref(self.cfg), C.byref(self.state), s.ctypes.data_as(C.POINTER(C.c_float)),
+                             s.shape[0], C.byref(g)))
+        return g.value
+
+    def snapshot(self) -> dict:
+        k = len(self.sizes)
+        st = self.state
+        return {"lambda": st.lam, "alpha": list(st.alpha[:k]), "beta": list(st.beta[:k]), "g_index": st.g_index,
+                "step": st.step, "last_rate": st.last_rate, "last_sample": list(st.last_sample[:k]),
+                "last_score": list(st.last_score[:k])}
+
+
+def sagc_beta_draw(seed: int, step: int, arm: int, a: float, b: float) -> float:
+    lib = load_library()
+    out = C.c_double()
+    _check(lib.sagc_beta_draw(C.c_uint64(seed & (2 ** 64 - 1)), step, arm, a, b, C.byref(out)))
+    return out.value

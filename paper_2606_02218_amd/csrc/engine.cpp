@@ -138,6 +138,9 @@ struct rg_policy {
   }
 };
 
+// Error reporting for the other host sources of the library.
+int rg_set_error(int code, const char* msg) { return fail(code, msg); }
+
 // ---------------------------------------------------------------- launch-event hook
 namespace {
 thread_local hipEvent_t g_arm_start = nullptr, g_arm_stop = nullptr;

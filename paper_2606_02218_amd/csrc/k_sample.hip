@@ -436,6 +436,63 @@ hipError_t launch_setup(const SetupArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ group length statistics
+// One 256-thread block per group: the group's offset is the sum of the sizes
+// before it; its lengths are ranked in LDS (rank = smaller values plus equal
+// values earlier in the group) and placed in sorted order.
+__global__ __launch_bounds__(256) void k_group_stats(const int32_t* __restrict__ lengths, const int32_t* __restrict__ G,
+                                                     int P, int N, double tau, float* __restrict__ stats) {
+  constexpr int GMAX = 1024;
+  __shared__ int s_len[GMAX], s_sorted[GMAX];
+  __shared__ unsigned long long s_off;
+  const int p = blockIdx.x, tid = threadIdx.x;
+  if (tid == 0) s_off = 0;
+  __syncthreads();
+  unsigned long long part = 0;
+  for (int i = tid; i < p; i += blockDim.x) part += (unsigned long long)(long long)G[i];
+  atomicAdd(&s_off, part);   // integer sum modulo 2^64: order-independent, exact for int32 sizes
+  __syncthreads();
+  const long long off = (long long)s_off;
+  const int g = G[p];
+  float* out = stats + 4 * (int64_t)p;
+  if (g < 1 || g > GMAX || off < 0 || off + g > N) {
+    if (tid < 4) out[tid] = NAN;
+    return;
+  }
+  for (int i = tid; i < g; i += blockDim.x) s_len[i] = lengths[off + i];
+  __syncthreads();
+  for (int i = tid; i < g; i += blockDim.x) {
+    const int v = s_len[i];
+    int rank = 0;
+    for (int j = 0; j < g; ++j) {
+      const int u = s_len[j];
+      rank += (u < v) || (u == v && j < i);
+    }
+    s_sorted[rank] = v;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int lmax = s_sorted[g - 1];
+    const double med = (g & 1) ? (double)s_sorted[g / 2] : ((double)s_sorted[g / 2 - 1] + (double)s_sorted[g / 2]) / 2.0;
+    if (!(med > 0.0)) {
+      out[0] = out[1] = out[2] = out[3] = NAN;
+      return;
+    }
+    const double R = (double)lmax / med;
+    out[0] = (float)lmax;
+    out[1] = (float)med;
+    out[2] = (float)R;
+    out[3] = R > tau ? 1.f : 0.f;
+  }
+}
+
+hipError_t launch_group_stats(const int32_t* lengths, const int32_t* G, int P, int N, double tau, float* stats,
+                              hipStream_t st) {
+  if (P < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_group_stats, dim3(P), dim3(256), 0, st, lengths, G, P, N, tau, stats);
+  return hipGetLastError();
+}
+
 hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P, int N, float eps, int ddof,
                                   float* adv, hipStream_t st) {
   hipLaunchKernelGGL(k_group_advantage, dim3(1), dim3(1024), 0, st, rewards, G, P, N, (double)eps, ddof, adv);

@@ -209,6 +209,13 @@ hipError_t launch_setup(const SetupArgs& a, hipStream_t st);
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st);
 
+// Per-group length summaries for the group-size controller: stats[p] =
+// (l_max, l_median, l_max / l_median, [l_max / l_median > tau]) of group p's
+// lengths (prompt-major, group sizes G, 1 <= G[p] <= 1024); NaN for a group
+// outside the bounds.
+hipError_t launch_group_stats(const int32_t* lengths, const int32_t* G, int P, int N, double tau, float* stats,
+                              hipStream_t st);
+
 hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P, int N, float eps,
                                   int ddof, float* adv, hipStream_t st);
 hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,
