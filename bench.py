@@ -94,6 +94,76 @@ def cpu_baseline(wl, weights, inputs, n_steps: int):
                       f"x {n_steps} decode steps ({gen} tokens) in {dt:.1f} s, float64 numpy"}
 
 
+def eb_sweep(args):
+    """Static G in {4, 8, 16} against the group-size controller at a fixed
+    effective batch of 64 sequences (B = 64 / G prompts per step), on the
+    1.5B-shaped policy.  Every training step is one rollout_group plus
+    group_advantage with fresh synthetic prompts, forced hierarchical-lognormal
+    lengths whose within-group spread narrows from 0.25 to 0.10 over the T
+    steps (the same schedule for every arm), and the per-group length
+    statistics computed on the GPU.  Prints one JSON line."""
+    import torch
+    import paper_2606_02218_amd as rg
+    from workload import get_config, make_weights, make_inputs, step_group_lengths, step_rewards
+
+    T, EB, sizes = args.eb_sweep, 64, (4, 8, 16)
+    wl = get_config(args.workload)
+    shape = wl.shape
+    pol = rg.Policy(shape, make_weights(shape, 0), max_seqs=EB, max_prompts=EB // min(sizes),
+                    max_prompt_tokens=EB // min(sizes) * wl.prompt_len, max_context=wl.prompt_len + wl.max_new)
+    pool = make_inputs(wl, 0).prompts
+    dev = torch.device("cuda")
+    out_tok = torch.empty((EB, wl.max_new), dtype=torch.int32, device=dev)
+    out_len = torch.empty(EB, dtype=torch.int32, device=dev)
+    out_lp = torch.empty((EB, wl.max_new), dtype=torch.float32, device=dev)
+    adv = torch.empty(EB, dtype=torch.float32, device=dev)
+
+    def train_step(t, G, ctl):
+        B = EB // G
+        sig = 0.25 + (0.10 - 0.25) * t / max(1, T - 1)
+        L = step_group_lengths(B, G, wl.max_new, 0, t, sig)
+        prompts = torch.from_numpy(pool[[(t * B + i) % len(pool) for i in range(B)]]).to(dev)
+        G_dev = torch.full((B,), G, dtype=torch.int32, device=dev)
+        rew = torch.from_numpy(step_rewards(B * G, 0, t)).to(dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pol.rollout(prompts, [G] * B, wl.max_new, 5000 + t, forced_len=L,
+                    out=(out_tok[:B * G], out_len[:B * G], out_lp[:B * G]))
+        rg.group_advantage(rew, G_dev, 1e-6, 1, out=adv[:B * G])
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        stats = ctl.group_stats(out_len[:B * G], G_dev).cpu().numpy()
+        return dt, stats, int(L.sum()), int(L.max())
+
+    warm = rg.Sagc(sizes=sizes)
+    train_step(0, 16, warm)                    # untimed: first-use set-up
+    arms = {}
+    for name in ("static-4", "static-8", "static-16", "sagc"):
+        ctl = rg.Sagc(sizes=sizes, seed=11)
+        G = int(name.split("-")[1]) if name != "sagc" else ctl.G
+        rec = {"G": [], "step_s": [], "straggler_rate": [], "tokens": 0, "max_len": []}
+        for t in range(T):
+            dt, stats, ntok, lmax = train_step(t, G, ctl)
+            rec["G"].append(G)
+            rec["step_s"].append(round(dt, 3))
+            rec["straggler_rate"].append(float(stats[:, 3].mean()))
+            rec["max_len"].append(lmax)
+            rec["tokens"] += ntok
+            if name == "sagc":
+                G = ctl.step(stats)
+            print(f"# {name} step {t}: G={rec['G'][-1]} {dt:.2f} s, straggler rate {rec['straggler_rate'][-1]:.2f}",
+                  file=sys.stderr, flush=True)
+        tot = sum(rec["step_s"])
+        rec.update({"mean_step_s": round(tot / T, 3), "tokens_per_s": round(rec["tokens"] / tot, 1),
+                    "straggler_pct": round(100 * float(np.mean(rec["straggler_rate"])), 1),
+                    "s_per_prompt": round(tot / sum(EB // g for g in rec["G"]), 4)})
+        if name == "sagc":
+            rec["controller"] = ctl.snapshot()
+        arms[name] = rec
+    print(json.dumps({"sweep": "static G vs group-size controller at EB = 64", "workload": wl.name,
+                      "steps_per_arm": T, "effective_batch": EB, "sizes": list(sizes), "arms": arms}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,6 +173,8 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
     ap.add_argument("--cpu-steps", type=int, default=32, help="decode steps of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eb-sweep", type=int, default=0, metavar="T",
+                    help="only run the static-G vs controller sweep at EB = 64 with T steps per arm and exit")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
     args = ap.parse_args()
@@ -115,6 +187,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calib_bytes_per_copy": n * 4, "copies": 5}))
+        return
+    if args.eb_sweep:
+        eb_sweep(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (groups would shard across GPUs "

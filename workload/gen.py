@@ -20,6 +20,7 @@ from .configs import ModelShape, Workload
 
 # stream ids: keep stable, they are part of the workload definition
 _S_WEIGHT, _S_PROMPT, _S_GROUP, _S_LEN, _S_REWARD_P, _S_REWARD = 11, 12, 13, 14, 15, 16
+_S_STEP_LEN, _S_STEP_REWARD = 17, 18
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 
@@ -172,3 +173,21 @@ def lognormal_cap_fraction(mu: float, sigma: float, cap: int) -> float:
     """P(exp(mu + sigma Z) + 0.5 >= cap): analytic fraction of capped lengths."""
     x = (math.log(cap - 0.5) - mu) / sigma
     return 0.5 * math.erfc(x / math.sqrt(2.0))
+
+
+def step_group_lengths(P: int, G: int, max_new: int, seed: int, step: int, sigma_w: float,
+                       mu: float = math.log(1200.0), sigma_p: float = 0.3) -> np.ndarray:
+    """Forced lengths [P*G] (prompt-major) of one training step of the
+    group-size sweep: prompt p has a typical length m_p = exp(mu + sigma_p z_p)
+    and its G completions floor(exp(log m_p + sigma_w z_pi) + 0.5), clipped to
+    [1, max_new].  sigma_w (within-group spread) sets the straggler rate."""
+    r = _rng(seed, _S_STEP_LEN, step)
+    zp = r.standard_normal(P)
+    zi = r.standard_normal((P, G))
+    L = np.floor(np.exp(mu + sigma_p * zp[:, None] + sigma_w * zi) + 0.5)
+    return np.clip(L, 1, max_new).astype(np.int32).reshape(-1)
+
+
+def step_rewards(n: int, seed: int, step: int, p: float = 0.5) -> np.ndarray:
+    """Bernoulli(p) rewards [n] of one training step of the group-size sweep."""
+    return (_rng(seed, _S_STEP_REWARD, step).random(n) < p).astype(np.float32)
