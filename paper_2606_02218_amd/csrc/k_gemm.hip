@@ -31,9 +31,8 @@
 
 namespace {
 
-constexpr int BK = 64;
+constexpr int BK_MAX = 64;             // K step of the small tiles; large tiles may use 32
 constexpr int LDS_PAD = 8;             // bf16 elements of padding per LDS row
-constexpr int LROW = BK + LDS_PAD;     // LDS row stride (elements)
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -126,12 +125,14 @@ __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, i
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
     const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep) {
   constexpr int WAVES_M = BM / (16 * WM), WAVES_N = BN / (16 * WN);
   constexpr int NT = WAVES_M * WAVES_N * 64;
+  constexpr int LROW = BK + LDS_PAD;                // LDS row stride (elements)
+  static_assert(BK == 32 || BK == 64, "K step");
   constexpr int A_PIECES = BM * (BK / 8);          // 16-byte pieces per A plane tile
   constexpr int W_PIECES = BN * (BK / 8);
   static_assert((2 * A_PIECES) % NT == 0 && W_PIECES % NT == 0, "tile pieces must split evenly over threads");
@@ -275,23 +276,59 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
 }
 
 // Residual add of the split partials followed by the next RMSNorm of the row
-// (x += sum; act = x / sqrt(mean(x^2) + eps) * g): one 256-thread block per row.
-template <int SPLIT>
-__global__ __launch_bounds__(512) void k_split_residual_norm(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+// (x += sum_s part_s; act = x / sqrt(mean(x^2) + eps) * g): one 1024-thread
+// block per row, thread t owning columns t + 1024 k (k < CPT).  A thread issues
+// its x and g loads and a batch of its split partials before the first add,
+// and the row stays in registers between the sum of squares and the store.
+// The sums run in split order, as in split_sum.
+template <int SPLIT, int CPT>
+__global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+  constexpr int NT = 1024;
+  constexpr int BATCH = CPT <= 2 ? 16 : 32 / CPT;   // splits loaded per batch
   const int r = blockIdx.x;
   if (r >= *d_rows) return;
   __shared__ float red[16];
   float* xr = ep.x + (int64_t)r * ep.ldx;
+  const float* pr = ep.part + (int64_t)r * N;
+  const int64_t pst = ep.part_stride;
+  float xv[CPT], gv[CPT], acc[CPT];
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    const int c = threadIdx.x + k * NT;
+    xv[k] = c < N ? xr[c] : 0.f;
+    gv[k] = c < N ? ep.norm_g[c] : 0.f;
+    acc[k] = 0.f;
+  }
+  for (int s0 = 0; s0 < S; s0 += BATCH) {
+    float t[BATCH][CPT];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j)
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) {
+        const int c = threadIdx.x + k * NT;
+        t[j][k] = (s0 + j < S && c < N) ? pr[(s0 + j) * pst + c] : 0.f;
+      }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j)
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) acc[k] += t[j][k];
+  }
   float ss = 0.f;
-  for (int c = threadIdx.x; c < N; c += blockDim.x) {
-    const float v = xr[c] + split_sum(ep, S, (int64_t)r * N + c);
-    xr[c] = v;
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    xv[k] += acc[k];
+    ss = fmaf(xv[k], xv[k], ss);
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)N + ep.norm_eps);
-  for (int c = threadIdx.x; c < N; c += blockDim.x)
-    act_store<SPLIT>(ep.norm_out, (int64_t)r * N + c, xr[c] * inv * ep.norm_g[c]);
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    const int c = threadIdx.x + k * NT;
+    if (c < N) {
+      xr[c] = xv[k];
+      act_store<SPLIT>(ep.norm_out, (int64_t)r * N + c, xv[k] * inv * gv[k]);
+    }
+  }
 }
 
 // Sum of split partials + epilogue: one block of 128 threads per (128
@@ -320,13 +357,13 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
   C[(int64_t)r * N + n] = acc;
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES>
+template <int BM, int BN, int WM, int WN, int STAGES, int BK = 64>
 hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
                         int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   constexpr int NT = (BM / (16 * WM)) * (BN / (16 * WN)) * 64;
   dim3 grid((N + BN - 1) / BN, (rows_ub + BM - 1) / BM, splits);
 #define RG_TILED(E)                                                                                           \
-  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, E>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane, \
+  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E>), grid, dim3(NT), 0, st, (const bf16_t*)A, lda, a_plane, \
                      (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep)
   if (splits > 1) {
     RG_TILED(GEMM_EPI_PARTIAL);
@@ -346,7 +383,14 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
 template <int SPLIT, typename KV>
 hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, const GemmEpi& ep, hipStream_t st) {
   if (ep.mode == GEMM_EPI_RESIDUAL && ep.norm_g) {
-    hipLaunchKernelGGL((k_split_residual_norm<SPLIT>), dim3(rows_ub), dim3(512), 0, st, d_rows, N, S, ep);
+    const int cpt = (N + 1023) / 1024;
+#define RG_SRN(C) hipLaunchKernelGGL((k_split_residual_norm<SPLIT, C>), dim3(rows_ub), dim3(1024), 0, st, d_rows, N, S, ep)
+    if (cpt <= 1) RG_SRN(1);
+    else if (cpt <= 2) RG_SRN(2);
+    else if (cpt <= 4) RG_SRN(4);
+    else if (cpt <= 8) RG_SRN(8);
+    else return hipErrorInvalidValue;   // rows wider than 8192
+#undef RG_SRN
     return hipGetLastError();
   }
   dim3 grid((N + 127) / 128, rows_ub);
@@ -385,7 +429,7 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
   if (ep.mode == GEMM_EPI_QKV && (ep.hd % 32 || 128 % ep.hd)) return hipErrorInvalidValue;
   hipError_t e;
   if (dtype == 1) {
-    if (K % BK || k_per_split % BK || N % 16) return hipErrorInvalidValue;
+    if (K % BK_MAX || k_per_split % BK_MAX || N % 16) return hipErrorInvalidValue;
     switch (gemm_tile_rows(dtype, rows_ub)) {
       case 16: e = launch_tiled<16, 128, 1, 2, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 32: e = launch_tiled<32, 128, 1, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;

@@ -68,18 +68,6 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, co
   for (int i = threadIdx.x; i < d; i += blockDim.x) act_store<SPLIT>(out, (int64_t)r * d + i, xr[i] * inv * g[i]);
 }
 
-__global__ void k_residual(const float* __restrict__ C, int64_t split_stride, int splits, int N, float* __restrict__ x,
-                           const int* __restrict__ d_rows) {
-  const int r = blockIdx.y;
-  if (r >= *d_rows) return;
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
-  const int64_t o = (int64_t)r * N + n;
-  float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += C[s * split_stride + o];
-  x[o] += v;
-}
-
 template <typename KV>
 __global__ void k_page_copy(KV* __restrict__ pool, int64_t page_elems, const int32_t* __restrict__ pairs,
                             const int32_t* __restrict__ state) {
@@ -166,19 +154,6 @@ hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, floa
   else
     hipLaunchKernelGGL(k_rmsnorm<0>, dim3(rows_ub), dim3(256), 0, st, x, g, d, eps, o, src_rows, d_rows);
   return hipGetLastError();
-}
-
-hipError_t launch_residual_norm(int dtype, const float* C, int64_t split_stride, int splits, int N, float* x,
-                                const float* g, float eps, void* out, int64_t a_plane, const int* d_rows,
-                                int rows_ub, hipStream_t st) {
-  if (rows_ub <= 0) return hipSuccess;
-  if (C) {
-    hipLaunchKernelGGL(k_residual, dim3((N + 255) / 256, rows_ub), dim3(256), 0, st, C, split_stride, splits, N, x,
-                       d_rows);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !g) return e;
-  }
-  return launch_rmsnorm(dtype, x, g, N, eps, out, a_plane, nullptr, d_rows, rows_ub, st);
 }
 
 hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs, int max_pairs,

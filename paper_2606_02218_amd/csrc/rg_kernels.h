@@ -134,13 +134,6 @@ hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_m
                              int head_dim, const int32_t* row_pos, const int32_t* row_beg, AttPlan plan, void* out,
                              int64_t a_plane, const int* d_rows, int rows_ub, hipStream_t st);
 
-// x[r][n] += sum_s C[s][r][n] (C may be NULL: no add; one block per 256
-// columns of a row), then, if g != NULL, out[r] = x[r] / sqrt(mean(x[r]^2) +
-// eps) * g as an activation operand (one block per row).
-hipError_t launch_residual_norm(int dtype, const float* C, int64_t split_stride, int splits, int N, float* x,
-                                const float* g, float eps, void* out, int64_t a_plane, const int* d_rows,
-                                int rows_ub, hipStream_t st);
-
 struct SampleArgs {
   const float* logits;      // [rows][V] or [P][V] when logits_by_group
   int logits_by_group;      // step 0: logits row = seq_grp[s]
