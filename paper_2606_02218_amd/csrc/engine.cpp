@@ -43,7 +43,7 @@ constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
 constexpr int RG_SPLIT_MAX = GEMM_MAX_SPLITS;   // largest split-K factor of a decode GEMM
 constexpr int RG_GEMM_TARGET = 384;    // blocks a split-K GEMM launch aims for
 constexpr int RG_GEMM_FULL = 256;      // output-tile blocks that need no split
-constexpr int RG_ATT_TARGET = 4096;    // work items an attention launch aims for
+constexpr int RG_ATT_TARGET = 1024;    // work items (waves) an attention launch aims for
 constexpr int RG_PRE_TARGET = 512;     // workgroups the prefix attention pass aims for
 constexpr int RG_PRE_MIN_CHUNK = 64;   // fewest prefix tokens per prefix workgroup
 constexpr int RG_PRE_MAX_SLOTS = 16;   // prefix chunks per row (more only for prefixes > 16k tokens)
@@ -283,11 +283,12 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
                const PrefixPass* pre) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
-  // chunks per row: enough work items to cover the chip, at least ~256 tokens
-  // each for the longest context, at most 16384 tokens each
-  int n_chunks = 1;
-  if ((int64_t)rows_ub * pol->nkv < RG_ATT_TARGET)
-    n_chunks = (int)std::min<int64_t>(ceil_div(RG_ATT_TARGET, (int64_t)rows_ub * pol->nkv), ceil_div(ctx_max, 256));
+  // chunks per row: about RG_ATT_TARGET work items (fewer, longer chunks
+  // measured faster than filling every wave slot: less partial traffic and
+  // per-item set-up), at least ~256 tokens each for the longest context, at
+  // most 16384 tokens each
+  const int64_t items = (int64_t)rows_ub * pol->nkv;
+  int n_chunks = (int)std::min<int64_t>((RG_ATT_TARGET + items / 2) / items, ceil_div(ctx_max, 256));
   n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16000)});
   AttPlan plan{n_chunks, 0, 0, n_chunks};
   if (pre && pre->max_pref > 0) {
@@ -325,9 +326,10 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
                                                 pol->att_o, pol->att_ml, st));
     LAUNCH_TIMED(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                        pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, pol->row_beg, ctx_max,
-                                       plan, pol->att_o, pol->att_ml, d_rows, rows_ub, st));
-    LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
-                                              pol->row_beg, plan, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+                                       plan, pol->att_o, pol->att_ml, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+    if (plan.n_slots > 1 || pol->dtype != RG_DTYPE_BF16)   // one bf16 slot: the attention wrote abuf2 itself
+      LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
+                                                pol->row_beg, plan, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
     // O projection + residual, then the MLP norm into abuf (fused into the
     // split epilogue when K is split)
     int S;

@@ -357,7 +357,8 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
                                                        const int32_t* __restrict__ row_pos,
                                                        const int32_t* __restrict__ row_beg, AttPlan plan,
                                                        int rows_ub, float* __restrict__ part_o,
-                                                       float* __restrict__ part_ml, const int* __restrict__ d_rows) {
+                                                       float* __restrict__ part_ml, ActOut out,
+                                                       const int* __restrict__ d_rows) {
   static_assert(HD % 32 == 0 && HD <= 256, "head_dim");
   // XCD-aware order: the 1-D grid has a multiple of 8 blocks and blocks are
   // dealt to the 8 XCDs round-robin, so XCD x = b % 8 takes the contiguous
@@ -433,9 +434,27 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
     if (t0 + 64 < c1) att_load<HD>(ba, pool, g, koff, voff, spg, c0, c1, t0 + 64, col, grp);
     step(bb, t0 + 32);
   }
-  if (col < rep)
-    att_store<HD>(st, ((int64_t)r * plan.n_slots + plan.pre_slots + chunk) * n_q + kvh * rep + col, grp, part_o,
-                  part_ml);
+  if (col < rep) {
+    if (plan.n_slots == 1) {   // the whole context in one work item: normalise and write the activation
+      const float inv = 1.0f / st.l;
+      bf16_t* o = (bf16_t*)out.base + ((int64_t)r * n_q + kvh * rep + col) * HD + 4 * grp;
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) {
+        uint32_t h[2], l[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const float v0 = st.o[dt][2 * e] * inv, v1 = st.o[dt][2 * e + 1] * inv;
+          h[e] = pack_bf16x2(v0, v1);
+          l[e] = pack_bf16x2(v0 - __uint_as_float(h[e] << 16), v1 - __uint_as_float(h[e] & 0xFFFF0000u));
+        }
+        *reinterpret_cast<uint2*>(o + dt * 16) = uint2{h[0], h[1]};
+        *reinterpret_cast<uint2*>(o + out.plane + dt * 16) = uint2{l[0], l[1]};
+      }
+    } else {
+      att_store<HD>(st, ((int64_t)r * plan.n_slots + plan.pre_slots + chunk) * n_q + kvh * rep + col, grp, part_o,
+                    part_ml);
+    }
+  }
 }
 
 
@@ -614,8 +633,8 @@ void att_launch(F kernel, dim3 grid, dim3 block, hipStream_t st, Args... args) {
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool,
                             KvGeom g, int layer, const int32_t* page_tab, int tab_stride,
                             const int32_t* row_tab, const int32_t* row_pos, const int32_t* row_beg, int max_ctx,
-                            AttPlan plan, float* part_o, float* part_ml, const int* d_rows, int rows_ub,
-                            hipStream_t st) {
+                            AttPlan plan, float* part_o, float* part_ml, void* out, int64_t a_plane,
+                            const int* d_rows, int rows_ub, hipStream_t st) {
   const int n_chunks = plan.n_chunks;
   if (n_chunks < 1 || plan.n_slots != plan.pre_slots + n_chunks || plan.n_slots > ATT_MAX_MERGE ||
       std::max(128, (max_ctx + n_chunks - 1) / n_chunks + 31) > 16 * ATT_MAX_CHUNK_PAGES)
@@ -629,7 +648,7 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
     att_launch(k_attention_mfma<HD>, grid1, dim3(64), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, page_tab, \
-               tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, d_rows)
+               tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, ActOut{out, a_plane}, d_rows)
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;

@@ -112,12 +112,14 @@ struct AttPlan {
 // row_tab[r] (at most max_ctx tokens), cut into n_chunks equal chunks
 // (rounded up to 32 tokens); each (row, kv head, chunk) work item writes a
 // partial (max, sum, unnormalised output) per query head.  row_beg[r] is a
-// multiple of 16.
+// multiple of 16.  bf16 models with a single slot (plan.n_slots == 1) write
+// the normalised output straight into the activation planes `out` instead
+// (no merge needed).
 hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int head_dim,
                             const void* kv_pool, KvGeom g, int layer, const int32_t* page_tab,
                             int tab_stride, const int32_t* row_tab, const int32_t* row_pos, const int32_t* row_beg,
-                            int max_ctx, AttPlan plan, float* part_o, float* part_ml, const int* d_rows,
-                            int rows_ub, hipStream_t st);
+                            int max_ctx, AttPlan plan, float* part_o, float* part_ml, void* out, int64_t a_plane,
+                            const int* d_rows, int rows_ub, hipStream_t st);
 
 // Prefix pass (bf16 models).  The active rows of prompt p are grp_row0[p] ..
 // grp_row1[p]-1 (empty when equal); all of them attend to positions
