@@ -32,7 +32,7 @@
 namespace {
 
 constexpr int BK_MAX = 64;             // K step of the small tiles; large tiles may use 32
-constexpr int LDS_PAD = 8;             // bf16 elements of padding per LDS row
+constexpr int LDS_PAD = 16;            // bf16 elements of padding per LDS row (rows 160 B apart: no bank conflicts)
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
