@@ -14,6 +14,8 @@
  *                       Gumbel-max from a Philox4x64-10 stream and retiring
  *                       every sequence at its EOS.
  *   group_advantage  -- A_i = (r_i - mean_g r) / (std_g r + eps) per group.
+ *   group_filter     -- which groups carry a learning signal (rewards not all
+ *                       equal), for DAPO-style dynamic sampling.
  *
  * Conventions for every entry point.
  *   - Status: 0 on success, a negative RG_E* code on error; rg_last_error()
@@ -191,6 +193,23 @@ int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N
                     int32_t ddof, float* adv, void* stream);
 
 /* ---- test and measurement hooks ---- */
+
+/* Zero-variance group filter (DAPO-style dynamic sampling, which the paper
+ * cites in Sec. 2 and uses in Sec. 5.1 without describing it): a group whose
+ * rewards are all equal (exact fp32 equality) has A = 0 for every member
+ * (see group_advantage) and gives no learning signal, so a trainer drops it
+ * and samples further prompts in its place.
+ *   rewards   DEVICE fp32 [N], groups back to back (N = sum(G))
+ *   G         DEVICE int32 [P], each >= 1
+ *   keep      DEVICE int32 [P]: 1 if group p's rewards vary, else 0
+ *   kept_ids  DEVICE int32 [P]: ids of the kept groups, ascending, in the
+ *             first n_kept entries
+ *   n_kept    DEVICE int32 [1]: the number of kept groups; -1 if a G[]
+ *             entry is < 1 or sum(G) != N (then nothing else is written)
+ * Only enqueues work on `stream`; allocates nothing.  RG_EINVAL for NULL
+ * pointers, P < 1 or N < 1. */
+int group_filter(const float* rewards, const int32_t* G, int32_t P, int32_t N, int32_t* keep,
+                 int32_t* kept_ids, int32_t* n_kept, void* stream);
 
 /* Raw Philox4x64-10 blocks: out[4i..4i+3] = Philox(ctr[4i..4i+3], key (key0, key1)).
  * ctr and out are DEVICE uint64 [4n].  Enqueue only. */

@@ -20,7 +20,7 @@ KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge"
 
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
            "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
-           "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw"]
+           "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter"]
 SAGC_MAX_SIZES = 8
 
 
@@ -96,6 +96,8 @@ def load_library():
     lib.rg_gumbel_bits.argtypes = [C.c_uint64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
     lib.rg_step_history.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rg_kernel_times.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    lib.group_filter.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                 C.c_void_p]
     lib.sagc_init.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state)]
     lib.sagc_group_stats.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p,
                                      C.c_void_p]
@@ -257,6 +259,20 @@ def group_advantage(rewards, G_dev, eps: float = 1e-6, ddof: int = 1, out=None, 
     _check(lib.group_advantage(_ptr(rewards), _ptr(G_dev), int(G_dev.numel()), int(rewards.numel()), float(eps),
                                int(ddof), _ptr(out), _stream_ptr(stream)))
     return out
+
+
+def group_filter(rewards, G_dev, stream=None):
+    """rewards: device fp32 [N]; G_dev: device int32 [P].  Returns device
+    tensors (keep [P], kept_ids [P], n_kept [1]) as written by the library."""
+    import torch
+    lib = load_library()
+    P = int(G_dev.numel())
+    keep = torch.empty(P, dtype=torch.int32, device=rewards.device)
+    kept = torch.full((P,), -1, dtype=torch.int32, device=rewards.device)
+    n = torch.empty(1, dtype=torch.int32, device=rewards.device)
+    _check(lib.group_filter(_ptr(rewards), _ptr(G_dev), P, int(rewards.numel()), _ptr(keep), _ptr(kept), _ptr(n),
+                            _stream_ptr(stream)))
+    return keep, kept, n
 
 
 def philox_blocks(key0: int, key1: int, ctr, stream=None):

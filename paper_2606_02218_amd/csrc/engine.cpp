@@ -853,6 +853,15 @@ int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N
   return RG_OK;
 }
 
+int group_filter(const float* rewards, const int32_t* G, int32_t P, int32_t N, int32_t* keep, int32_t* kept_ids,
+                 int32_t* n_kept, void* stream) {
+  if (!rewards || !G || !keep || !kept_ids || !n_kept) return fail(RG_EINVAL, "group_filter: NULL argument");
+  if (P < 1 || N < 1) return fail(RG_EINVAL, "group_filter: P < 1 or N < 1");
+  hipError_t e = launch_group_filter(rewards, G, P, N, keep, kept_ids, n_kept, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("group_filter launch: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
 int rg_philox_blocks(uint64_t key0, uint64_t key1, const uint64_t* ctr, int64_t n, uint64_t* out, void* stream) {
   if (!ctr || !out || n < 0) return fail(RG_EINVAL, "rg_philox_blocks: bad argument");
   hipError_t e = launch_philox_blocks(key0, key1, ctr, n, out, (hipStream_t)stream);

@@ -30,6 +30,29 @@ __device__ int block_excl_scan(int v, int* lds, int* total) {
   return excl;
 }
 
+// 1 when every G[p] >= 1 and sum(G) == N, summed in 64 bits so that no
+// choice of G can wrap around to a false match.  Block-wide: every thread of
+// the block calls it and gets the same answer.
+__device__ bool groups_valid(const int32_t* __restrict__ G, int P, int N) {
+  __shared__ unsigned long long s_sum;
+  __shared__ int s_bad;
+  if (threadIdx.x == 0) { s_sum = 0; s_bad = 0; }
+  __syncthreads();
+  long long loc = 0;
+  int bad = 0;
+  for (int p = threadIdx.x; p < P; p += blockDim.x) {
+    const int g = G[p];
+    bad |= g < 1;
+    loc += g;
+  }
+  if (bad) atomicOr(&s_bad, 1);
+  atomicAdd(&s_sum, (unsigned long long)loc);
+  __syncthreads();
+  const bool ok = !s_bad && s_sum == (unsigned long long)N;
+  __syncthreads();
+  return ok;
+}
+
 // ------------------------------------------------------------------ sampling
 // Two kernels.  k_sample_slice: block (slice, row) scans one slice of the
 // row's vocabulary -- Gumbel scores, running logsumexp of z/T -- and writes
@@ -341,21 +364,8 @@ __global__ __launch_bounds__(1024) void k_group_advantage(const float* __restric
                                                           int ddof, float* __restrict__ adv) {
   __shared__ int lds[17];
   __shared__ int offs[1025];
-  __shared__ int bad;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
-  if (tid == 0) bad = 0;
-  __syncthreads();
-  long long total = 0;
-  for (int base = 0; base < P; base += blockDim.x) {
-    const int p = base + tid;
-    const int g = p < P ? G[p] : 0;
-    if (p < P && g < 1) atomicOr(&bad, 1);
-    int t;
-    block_excl_scan(g < 0 ? 0 : g, lds, &t);
-    total += t;
-  }
-  __syncthreads();
-  if (bad || total != (long long)N) {
+  if (!groups_valid(G, P, N)) {
     for (int i = tid; i < N; i += blockDim.x) adv[i] = __int_as_float(0x7FC00000);
     return;
   }
@@ -490,6 +500,47 @@ hipError_t launch_group_stats(const int32_t* lengths, const int32_t* G, int P, i
                               hipStream_t st) {
   if (P < 1) return hipSuccess;
   hipLaunchKernelGGL(k_group_stats, dim3(P), dim3(256), 0, st, lengths, G, P, N, tau, stats);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ zero-variance filter
+// One block of 1024 threads.  Validates G as the advantage does; then, per
+// tile of 1024 groups, the block scan gives each group its offset, one thread
+// per group compares its rewards with the first one (exact fp32 equality),
+// and a second scan compacts the ids of the groups that vary.  n_kept[0] =
+// number of kept groups, or -1 when G is invalid (nothing else written).
+__global__ __launch_bounds__(1024) void k_group_filter(const float* __restrict__ rewards, const int32_t* __restrict__ G,
+                                                      int P, int N, int32_t* __restrict__ keep,
+                                                      int32_t* __restrict__ kept_ids, int32_t* __restrict__ n_kept) {
+  __shared__ int lds[17];
+  const int tid = threadIdx.x;
+  if (!groups_valid(G, P, N)) {
+    if (tid == 0) n_kept[0] = -1;
+    return;
+  }
+  int carry = 0, kcarry = 0;
+  for (int base = 0; base < P; base += blockDim.x) {
+    const int p = base + tid;
+    const int g = p < P ? G[p] : 0;
+    int t, kt;
+    const int o = block_excl_scan(g, lds, &t) + carry;
+    int varies = 0;
+    if (p < P) {
+      const float r0 = rewards[o];
+      for (int i = 1; i < g && !varies; ++i) varies = rewards[o + i] != r0;
+      keep[p] = varies;
+    }
+    const int k = block_excl_scan(varies, lds, &kt) + kcarry;
+    if (varies) kept_ids[k] = p;
+    carry += t;
+    kcarry += kt;
+  }
+  if (tid == 0) n_kept[0] = kcarry;
+}
+
+hipError_t launch_group_filter(const float* rewards, const int32_t* G, int P, int N, int32_t* keep, int32_t* kept_ids,
+                               int32_t* n_kept, hipStream_t st) {
+  hipLaunchKernelGGL(k_group_filter, dim3(1), dim3(1024), 0, st, rewards, G, P, N, keep, kept_ids, n_kept);
   return hipGetLastError();
 }
 

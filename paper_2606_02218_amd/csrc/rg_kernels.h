@@ -211,6 +211,8 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st);
 hipError_t launch_group_stats(const int32_t* lengths, const int32_t* G, int P, int N, double tau, float* stats,
                               hipStream_t st);
 
+hipError_t launch_group_filter(const float* rewards, const int32_t* G, int P, int N, int32_t* keep, int32_t* kept_ids,
+                               int32_t* n_kept, hipStream_t st);
 hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P, int N, float eps,
                                   int ddof, float* adv, hipStream_t st);
 hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,

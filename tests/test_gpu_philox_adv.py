@@ -1,10 +1,10 @@
 """GPU parity: Philox blocks and sampling bits bit-exact; group advantage
-within 1e-5 relative of the oracle."""
+within 1e-5 relative of the oracle; the zero-variance group filter bit-exact."""
 import numpy as np
 import pytest
 
 from oracle.philox import philox4x64_10, gumbel_uniform_bits
-from oracle.advantage import group_advantage as oracle_adv
+from oracle.advantage import group_advantage as oracle_adv, zero_variance_filter
 from workload import get_config, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -78,6 +78,60 @@ def test_advantage_workload_rewards(rg):
 def test_advantage_bad_group_sizes_give_nan(rg):
     import torch
     r = torch.ones(8, device="cuda")
-    for G in ([4, 3], [4, 0, 4], [4, 5]):
+    for G in ([4, 3], [4, 0, 4], [4, 5], [2 ** 31 - 1, 2 ** 31 - 1, 10]):
         out = rg.group_advantage(r, torch.tensor(G, dtype=torch.int32, device="cuda")).cpu().numpy()
         assert np.all(np.isnan(out)), G
+
+
+def _filter_case(rg, rewards, G):
+    import torch
+    r = torch.from_numpy(np.asarray(rewards, np.float32)).cuda()
+    keep, ids, n = rg.group_filter(r, torch.from_numpy(np.asarray(G, np.int32)).cuda())
+    ref_keep, ref_ids = zero_variance_filter(rewards, G)
+    n = int(n.item())
+    assert n == len(ref_ids)
+    np.testing.assert_array_equal(keep.cpu().numpy(), ref_keep)
+    ids = ids.cpu().numpy()
+    np.testing.assert_array_equal(ids[:n], ref_ids)
+    assert np.all(ids[n:] == -1)   # untouched past the kept count
+    return ref_keep
+
+
+def test_group_filter_layouts(rg):
+    rng = np.random.default_rng(11)
+    layouts = [[4] * 8, [16] * 32, list(make_inputs(get_config("1.5b-dyn"), 0).G), [1, 2, 3, 1000, 5],
+               list(rng.integers(1, 9, size=3000)), [1], [2] * 2049]
+    for G in layouts:
+        N = int(np.sum(G))
+        off = np.concatenate([[0], np.cumsum(G)])
+        r = (rng.random(N) < rng.random()).astype(np.float32)
+        _filter_case(rg, r, G)
+        r = rng.normal(size=N).astype(np.float32)
+        for p in range(0, len(G), 2):
+            r[off[p]:off[p + 1]] = r[off[p]]
+        keep = _filter_case(rg, r, G)
+        assert keep[::2].sum() == 0
+
+
+def test_group_filter_edge_values(rg):
+    G = [2, 2, 2, 1, 2, 3]
+    r = [0.0, -0.0, 1.0, float(np.nextafter(np.float32(1), np.float32(2))), np.nan, np.nan, np.nan, 5.0, 5.0,
+         np.inf, np.inf, np.inf]
+    _filter_case(rg, np.array(r, np.float32), G)
+    _filter_case(rg, np.ones(64, np.float32), [64])
+    _filter_case(rg, np.zeros(4096, np.float32), [1] * 4096)
+
+
+def test_group_filter_workload_rewards(rg):
+    for name in ["tiny", "gpt2s", "1.5b", "1.5b-dyn", "7b"]:
+        inp = make_inputs(get_config(name), 0)
+        _filter_case(rg, inp.rewards, list(inp.G))
+
+
+def test_group_filter_bad_group_sizes(rg):
+    import torch
+    r = torch.ones(8, device="cuda")
+    for G in ([4, 3], [4, 0, 4], [4, 5], [2 ** 31 - 1, 2 ** 31 - 1, 10]):
+        keep, ids, n = rg.group_filter(r, torch.tensor(G, dtype=torch.int32, device="cuda"))
+        assert int(n.item()) == -1, G
+        assert np.all(ids.cpu().numpy() == -1), G
