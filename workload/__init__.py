@@ -9,4 +9,5 @@ from .configs import CONFIGS, ModelShape, Workload, get_config  # noqa: F401
 from .gen import (  # noqa: F401
     make_weights, make_prompts, make_group_sizes, make_forced_lengths,
     make_rewards, make_inputs, bf16_round_f32, f32_to_bf16_bits, step_group_lengths, step_rewards,
+    drifted_logprobs,
 )

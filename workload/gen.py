@@ -20,7 +20,7 @@ from .configs import ModelShape, Workload
 
 # stream ids: keep stable, they are part of the workload definition
 _S_WEIGHT, _S_PROMPT, _S_GROUP, _S_LEN, _S_REWARD_P, _S_REWARD = 11, 12, 13, 14, 15, 16
-_S_STEP_LEN, _S_STEP_REWARD = 17, 18
+_S_STEP_LEN, _S_STEP_REWARD, _S_DRIFT = 17, 18, 19
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 
@@ -191,3 +191,14 @@ def step_group_lengths(P: int, G: int, max_new: int, seed: int, step: int, sigma
 def step_rewards(n: int, seed: int, step: int, p: float = 0.5) -> np.ndarray:
     """Bernoulli(p) rewards [n] of one training step of the group-size sweep."""
     return (_rng(seed, _S_STEP_REWARD, step).random(n) < p).astype(np.float32)
+
+
+def drifted_logprobs(logprobs: np.ndarray, lengths: np.ndarray, seed: int, scale: float = 0.1) -> np.ndarray:
+    """float32 [N, max_new]: a stand-in for the log-probabilities of an older
+    policy snapshot -- the given ones plus N(0, scale) noise at every valid
+    position (t < lengths[s]), zero elsewhere."""
+    lp = np.asarray(logprobs, np.float64)
+    N, T = lp.shape
+    noise = _rng(seed, _S_DRIFT).standard_normal((N, T)) * scale
+    valid = np.arange(T)[None, :] < np.asarray(lengths)[:, None]
+    return np.where(valid, lp + noise, 0.0).astype(np.float32)
