@@ -16,6 +16,9 @@
  *   group_advantage  -- A_i = (r_i - mean_g r) / (std_g r + eps) per group.
  *   group_filter     -- which groups carry a learning signal (rewards not all
  *                       equal), for DAPO-style dynamic sampling.
+ *   recompute_logprobs, grpo_surrogate -- the loss forward that follows:
+ *                       teacher-forced log-probabilities of the rollout under
+ *                       the policy and the clipped surrogate built on them.
  *
  * Conventions for every entry point.
  *   - Status: 0 on success, a negative RG_E* code on error; rg_last_error()
@@ -188,11 +191,9 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
  *   adv      DEVICE fp32 [N] (may not alias rewards)
  * Only enqueues work on `stream`; allocates nothing.  Errors: RG_EINVAL for
  * P < 1, N < 1, eps < 0 or ddof not in {0, 1}; a G[] entry < 1 or a sum that
- * differs from N makes the kernel write NaN to adv[0].  */
+ * differs from N makes the kernel write NaN to every adv[i].  */
 int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N, float eps,
                     int32_t ddof, float* adv, void* stream);
-
-/* ---- test and measurement hooks ---- */
 
 /* Zero-variance group filter (DAPO-style dynamic sampling, which the paper
  * cites in Sec. 2 and uses in Sec. 5.1 without describing it): a group whose
@@ -210,6 +211,64 @@ int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N
  * pointers, P < 1 or N < 1. */
 int group_filter(const float* rewards, const int32_t* G, int32_t P, int32_t N, int32_t* keep,
                  int32_t* kept_ids, int32_t* n_kept, void* stream);
+
+/* Teacher-forced log-probabilities of finished completions under the policy
+ * (the first half of the GRPO / DAPO loss forward, Sec. 2 and Sec. 5: the
+ * trainer scores the rollout under the current weights before its update).
+ * For every sequence s of prompt p and t < lengths[s]:
+ *   logprobs[s*max_new + t] = z_{y_t}/T - logsumexp(z/T),
+ * z the logits after the prompt and y_0 .. y_{t-1} = tokens[s*max_new ..].
+ * The prompts are prefilled once, the siblings fork over their shared prompt
+ * pages, and all completion positions then run as prefill-style rows (many
+ * positions per sequence per launch) through the same decoder kernels as the
+ * rollout, with the lm head in row slices and a fused logsumexp/gather.
+ *   prompts, prompt_len, P, G, max_new   as for rollout_group
+ *   tokens     DEVICE int32 [N*max_new], ids in [0, vocab) for t < lengths[s]
+ *   lengths    DEVICE int32 [N], each in [1, max_new]
+ *   temperature  > 0 (use the rollout's to reproduce its logprobs)
+ *   flags      RG_FLAG_PROFILE and RG_FLAG_NO_PREFIX_SHARING as in
+ *              rg_sampling.flags; profiled kernel times land in phase 0
+ *              (prompt prefill) and phase 1 (completion rows)
+ *   logprobs   DEVICE fp32 [N*max_new] out; 0 for t >= lengths[s]
+ * The KV pool must hold every completion position at once (the default pool
+ * does).  Returns after the stream has finished the work.  Errors: RG_EINVAL
+ * (arguments, a length outside [1, max_new], a token id outside [0, vocab)),
+ * RG_ENOMEM (limits or KV pool), RG_EHIP. */
+int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_len, int32_t P,
+                       const int32_t* G, const int32_t* tokens, const int32_t* lengths, int32_t max_new,
+                       float temperature, int32_t flags, float* logprobs, void* stream);
+
+/* Aggregation modes of grpo_surrogate */
+#define RG_LOSS_TOKEN_MEAN 0   /* DAPO: mean over every counted token                        */
+#define RG_LOSS_SEQ_MEAN   1   /* GRPO: mean over sequences of each sequence's token mean    */
+
+/* Clipped surrogate of the GRPO / DAPO objective (the PPO clip that both
+ * papers the method trains with use; the paper itself gives no formula).  Per
+ * token t < lengths[s]: rho = exp(new_lp - old_lp) and the term
+ * min(rho*A_s, clip(rho, 1 - eps_lo, 1 + eps_hi)*A_s), all in fp64; eps_lo =
+ * eps_hi is the PPO/GRPO clip, eps_hi > eps_lo DAPO's decoupled one.  No KL
+ * term.  Sequences of groups with keep[p] == 0 are left out.
+ *   new_lp, old_lp  DEVICE fp32 [N*max_new]
+ *   adv             DEVICE fp32 [N] (group_advantage's output)
+ *   lengths         DEVICE int32 [N], each in [1, max_new]
+ *   G               DEVICE int32 [P], each >= 1, sum N
+ *   keep            DEVICE int32 [P] (group_filter's keep) or NULL for all
+ *   out             DEVICE fp64 [4]: loss = -(aggregate of the terms), the
+ *                   fraction of counted tokens where the clip is active (the
+ *                   clipped term strictly below the unclipped one), the
+ *                   counted tokens and the counted sequences.  All zero when
+ *                   nothing is counted; NaN in all four if G is invalid or a
+ *                   length lies outside [1, max_new].
+ * One workgroup; the summation order is fixed, so results are reproducible.
+ * Only enqueues work on `stream`; allocates nothing.  Errors: RG_EINVAL for
+ * NULL pointers, P, N or max_new < 1, eps_lo outside [0, 1), eps_hi < 0 or an
+ * unknown mode. */
+int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
+                   const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep,
+                   double eps_lo, double eps_hi, int32_t mode, double* out, void* stream);
+
+/* ---- test and measurement hooks ---- */
+
 
 /* Raw Philox4x64-10 blocks: out[4i..4i+3] = Philox(ctr[4i..4i+3], key (key0, key1)).
  * ctr and out are DEVICE uint64 [4n].  Enqueue only. */
@@ -246,7 +305,8 @@ int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t
 #define RG_K_SAMPLE    12
 #define RG_K_COMPACT   13
 #define RG_K_SETUP     14
-#define RG_K_COUNT     15
+#define RG_K_LOGPROB   15   /* token log-probability gather of recompute_logprobs */
+#define RG_K_COUNT     16
 /* Totals for kernel class `kind` over the decode steps (phase 1) or the
  * prefill (phase 0) of the last profiled rollout: summed launch durations in
  * milliseconds (HIP events) and the number of launches. */

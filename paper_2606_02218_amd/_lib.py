@@ -16,12 +16,27 @@ RG_OK, RG_EINVAL, RG_ENOMEM, RG_EHIP, RG_EUNSUPPORTED = 0, -1, -2, -3, -4
 RG_DTYPE_F32, RG_DTYPE_BF16 = 0, 1
 RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE, RG_FLAG_GROUP_PREFIX = 1, 2, 4
 KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge", "gemm_o", "gemm_gu", "swiglu",
-                "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup"]
+                "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup", "logprob"]
 
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
            "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
-           "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter"]
+           "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter",
+           "recompute_logprobs", "grpo_surrogate"]
 SAGC_MAX_SIZES = 8
+
+
+def _pack_prompts(prompts):
+    """A device int32 [P, Lp] tensor or a list of 1-D ones -> (packed, lengths)."""
+    import torch
+    if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
+        plen = [prompts.shape[1]] * prompts.shape[0]
+        packed = prompts.contiguous().view(-1)
+    else:
+        plen = [int(p.numel()) for p in prompts]
+        packed = torch.cat([p.view(-1) for p in prompts])
+    if packed.dtype != torch.int32 or packed.device.type != "cuda":
+        raise TypeError("prompts must be int32 tensors on the GPU")
+    return packed, plen
 
 
 class RolloutError(RuntimeError):
@@ -98,6 +113,10 @@ def load_library():
     lib.rg_kernel_times.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
     lib.group_filter.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                  C.c_void_p]
+    lib.recompute_logprobs.argtypes = [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32),
+                                       C.c_void_p, C.c_void_p, C.c_int32, C.c_float, C.c_int32, C.c_void_p, C.c_void_p]
+    lib.grpo_surrogate.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
+                                   C.c_int32, C.c_void_p, C.c_double, C.c_double, C.c_int32, C.c_void_p, C.c_void_p]
     lib.sagc_init.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state)]
     lib.sagc_group_stats.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p,
                                      C.c_void_p]
@@ -191,14 +210,7 @@ class Policy:
         (RG_FLAG_GROUP_PREFIX)."""
         import torch
         lib = load_library()
-        if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
-            plen = [prompts.shape[1]] * prompts.shape[0]
-            packed = prompts.contiguous().view(-1)
-        else:
-            plen = [int(p.numel()) for p in prompts]
-            packed = torch.cat([p.view(-1) for p in prompts])
-        if packed.dtype != torch.int32 or packed.device.type != "cuda":
-            raise TypeError("prompts must be int32 tensors on the GPU")
+        packed, plen = _pack_prompts(prompts)
         P = len(plen)
         G = [int(g) for g in G]
         N = sum(G)
@@ -232,6 +244,29 @@ class Policy:
             return tokens, lengths, logprobs, dump
         return tokens, lengths, logprobs
 
+    def recompute_logprobs(self, prompts, G: Sequence[int], tokens, lengths, temperature: float = 1.0,
+                           share_prefix: bool = True, profile: bool = False, out=None, stream=None):
+        """Teacher-forced log-probabilities [N, max_new] of the completions
+        ``tokens`` (device int32 [N, max_new]) with ``lengths`` (device int32
+        [N]) after ``prompts`` (as for ``rollout``)."""
+        import torch
+        lib = load_library()
+        packed, plen = _pack_prompts(prompts)
+        P = len(plen)
+        G = [int(g) for g in G]
+        N, max_new = int(tokens.shape[0]), int(tokens.shape[1])
+        if N != sum(G):
+            raise ValueError("tokens must have sum(G) rows")
+        tokens = tokens.to(dtype=torch.int32).contiguous()
+        lengths = lengths.to(dtype=torch.int32).contiguous()
+        lp = torch.empty((N, max_new), dtype=torch.float32, device=packed.device) if out is None else out
+        flags = (0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+        plen_a = (C.c_int32 * P)(*plen)
+        g_a = (C.c_int32 * P)(*G)
+        _check(lib.recompute_logprobs(self._h, _ptr(packed), plen_a, P, g_a, _ptr(tokens), _ptr(lengths), max_new,
+                                      float(temperature), flags, _ptr(lp), _stream_ptr(stream)))
+        return lp
+
     def step_history(self, cap: int = 1 << 16):
         lib = load_library()
         n = C.c_int32()
@@ -258,6 +293,23 @@ def group_advantage(rewards, G_dev, eps: float = 1e-6, ddof: int = 1, out=None, 
         out = torch.empty_like(rewards)
     _check(lib.group_advantage(_ptr(rewards), _ptr(G_dev), int(G_dev.numel()), int(rewards.numel()), float(eps),
                                int(ddof), _ptr(out), _stream_ptr(stream)))
+    return out
+
+
+LOSS_MODES = {"token": 0, "seq": 1}
+
+
+def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps_hi: float = 0.2,
+                   mode: str = "token", keep=None, stream=None):
+    """Clipped surrogate; returns a device fp64 tensor (loss, clipped
+    fraction, counted tokens, counted sequences)."""
+    import torch
+    lib = load_library()
+    N, max_new = int(new_lp.shape[0]), int(new_lp.shape[1])
+    out = torch.empty(4, dtype=torch.float64, device=new_lp.device)
+    _check(lib.grpo_surrogate(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()),
+                              N, max_new, _ptr(keep), float(eps_lo), float(eps_hi), LOSS_MODES[mode], _ptr(out),
+                              _stream_ptr(stream)))
     return out
 
 

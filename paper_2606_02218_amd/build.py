@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librollout.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["k_gemm.hip", "k_attn.hip", "k_misc.hip", "k_sample.hip", "engine.cpp", "sagc.cpp"]
+SOURCES = ["k_gemm.hip", "k_attn.hip", "k_misc.hip", "k_sample.hip", "k_loss.hip", "engine.cpp", "sagc.cpp"]
 ARCH = os.environ.get("RG_OFFLOAD_ARCH", "gfx950")
 
 

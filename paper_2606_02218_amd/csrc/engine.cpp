@@ -93,7 +93,7 @@ struct rg_policy {
           *act_seq = nullptr, *act_tok = nullptr, *done = nullptr, *row_tab = nullptr, *row_pos = nullptr,
           *free_stack = nullptr, *state = nullptr, *copy_pairs = nullptr, *last_rows = nullptr,
           *hist_active = nullptr, *hist_groups = nullptr, *row_beg = nullptr, *grp_row0 = nullptr,
-          *grp_row1 = nullptr;
+          *grp_row1 = nullptr, *coff = nullptr, *row_tgt = nullptr, *row_out = nullptr, *row_lrow = nullptr;
   int64_t* hist_ctx = nullptr;
   int hist_cap = 0;
 
@@ -428,6 +428,124 @@ int step_graph(rg_policy* pol, StepGraphs& gs, int rows_ub, int ctx_max, const S
   return RG_OK;
 }
 
+// Prompts and group sizes of one call, checked against the policy's limits.
+struct GroupRun {
+  int P = 0, N = 0, max_plen = 0, T_pre = 0;
+};
+
+int check_groups(const rg_policy* pol, const char* who, const int32_t* prompt_len, int32_t P, const int32_t* G,
+                 int32_t max_new, GroupRun* gr) {
+  const rg_limits& lim = pol->lim;
+  const std::string w(who);
+  if (P < 1) return fail(RG_EINVAL, w + ": P < 1");
+  if (max_new < 1) return fail(RG_EINVAL, w + ": max_new < 1");
+  if (P > lim.max_prompts) return fail(RG_ENOMEM, w + ": P exceeds limits.max_prompts");
+  int64_t N = 0, T_pre = 0, pre_pages = 0;
+  int max_plen = 0;
+  for (int p = 0; p < P; ++p) {
+    if (prompt_len[p] < 1) return fail(RG_EINVAL, w + ": prompt_len < 1");
+    if (G[p] < 1) return fail(RG_EINVAL, w + ": G < 1");
+    N += G[p];
+    T_pre += prompt_len[p];
+    max_plen = std::max(max_plen, prompt_len[p]);
+    pre_pages += ceil_div(prompt_len[p], pol->page_tok);
+  }
+  if (N > lim.max_seqs) return fail(RG_ENOMEM, w + ": sum(G) exceeds limits.max_seqs");
+  if (T_pre > lim.max_prompt_tokens) return fail(RG_ENOMEM, w + ": prompt tokens exceed limits");
+  if ((int64_t)max_plen + max_new > lim.max_context) return fail(RG_ENOMEM, w + ": context exceeds limits");
+  if (pre_pages > pol->pool_pages) return fail(RG_ENOMEM, w + ": prompt pages exceed the KV pool");
+  gr->P = P; gr->N = (int)N; gr->max_plen = max_plen; gr->T_pre = (int)T_pre;
+  return RG_OK;
+}
+
+// Copies prompt lengths, G and (when given) per-sequence forced lengths into
+// device memory through the pinned staging buffer.
+int stage_groups(rg_policy* pol, hipStream_t st, const GroupRun& gr, const int32_t* prompt_len, const int32_t* G,
+                 const int32_t* forced_len) {
+  int32_t* hs = pol->h_stage;
+  HIPTRY(hipStreamSynchronize(st));   // the staging buffer may still feed an earlier call's copies
+  std::memcpy(hs, prompt_len, (size_t)gr.P * 4);
+  std::memcpy(hs + gr.P, G, (size_t)gr.P * 4);
+  HIPTRY(hipMemcpyAsync(pol->plen, hs, (size_t)gr.P * 4, hipMemcpyHostToDevice, st));
+  HIPTRY(hipMemcpyAsync(pol->G_dev, hs + gr.P, (size_t)gr.P * 4, hipMemcpyHostToDevice, st));
+  if (forced_len) {
+    std::memcpy(hs + 2 * gr.P, forced_len, (size_t)gr.N * 4);
+    HIPTRY(hipMemcpyAsync(pol->seq_forced, hs + 2 * gr.P, (size_t)gr.N * 4, hipMemcpyHostToDevice, st));
+  }
+  return RG_OK;
+}
+
+// Set-up (offsets, prompt page tables, free stack, output padding), the
+// prefill of every prompt (pol->logits then holds each prompt's
+// last-position logits) and the sibling fork with its copy-on-write pages.
+// tokens_out may be NULL (left untouched).
+int prefill_and_fork(rg_policy* pol, hipStream_t st, const GroupRun& gr, const int32_t* prompts,
+                     const int32_t* prompt_len, const int32_t* G, int32_t max_new, bool share, int32_t* tokens_out,
+                     float* logprobs_out) {
+  const int P = gr.P, N = gr.N;
+  SetupArgs sa{};
+  sa.P = P; sa.n_seq = N; sa.max_new = max_new; sa.page_tok = pol->page_tok; sa.max_pages = pol->max_pages;
+  sa.pool_pages = pol->pool_pages; sa.plen = pol->plen; sa.prompt_off = pol->prompt_off; sa.grp_off = pol->grp_off;
+  sa.G = pol->G_dev; sa.page_tab = pol->page_tab; sa.free_stack = pol->free_stack; sa.state = pol->state;
+  sa.tokens_out = tokens_out; sa.logprobs_out = logprobs_out; sa.last_rows = pol->last_rows;
+  LAUNCH(RG_K_SETUP, launch_setup(sa, st));
+
+  const int* d_pre = pol->state + 5;
+  LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, N, pol->row_tab, pol->row_pos, pol->row_beg, gr.T_pre,
+                                         st));
+  LAUNCH(RG_K_EMBED, launch_embed(pol->dtype, pol->w_embed, pol->d, pol->V, prompts, pol->x, pol->state + 7, d_pre,
+                                  gr.T_pre, st));
+  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                       pol->a_plane, nullptr, d_pre, gr.T_pre, st));
+  int rc = run_layers(pol, st, d_pre, gr.T_pre, gr.max_plen, false, nullptr);
+  if (rc) return rc;
+  if ((rc = run_head(pol, st, pol->state + 6, P, pol->last_rows))) return rc;
+
+  ForkArgs fa{};
+  fa.P = P; fa.n_seq = N; fa.page_tok = pol->page_tok; fa.max_pages = pol->max_pages;
+  fa.share = share ? 1 : 0;
+  fa.grp_off = pol->grp_off; fa.plen = pol->plen; fa.page_tab = pol->page_tab; fa.seq_grp = pol->seq_grp;
+  fa.seq_npages = pol->seq_npages; fa.seq_nshared = pol->seq_nshared; fa.act_seq = pol->act_seq;
+  fa.free_stack = pol->free_stack; fa.state = pol->state; fa.copy_pairs = pol->copy_pairs;
+  LAUNCH(RG_K_SETUP, launch_fork(fa, st));
+  int max_pairs = 0;
+  for (int p = 0; p < P; ++p) {
+    const int n_pref = (int)ceil_div(prompt_len[p], pol->page_tok);
+    const int need = share ? (prompt_len[p] % pol->page_tok ? 1 : 0) : n_pref;
+    max_pairs += need * G[p];
+  }
+  LAUNCH(RG_K_SETUP, launch_page_copy(pol->dtype, pol->kv_pool, pol->geom.page_elems, pol->copy_pairs, max_pairs,
+                                      pol->state, st));
+  return RG_OK;
+}
+
+// Profiling state of a call that takes RG_FLAG_PROFILE.
+int prof_begin(rg_policy* pol, bool on, uint32_t kinds) {
+  pol->prof = on;
+  pol->prof_mask = kinds ? kinds : 0xFFFFFFFFu;
+  if (pol->prof) {
+    if (pol->prof_ev.empty()) {
+      pol->prof_ev.resize(2 * RG_PROF_RING);
+      pol->prof_kind.resize(RG_PROF_RING);
+      pol->prof_ph.resize(RG_PROF_RING);
+      for (auto& e : pol->prof_ev) HIPTRY(hipEventCreate(&e));
+    }
+    std::memset(pol->kt_ms, 0, sizeof(pol->kt_ms));
+    std::memset(pol->kt_n, 0, sizeof(pol->kt_n));
+    pol->prof_head = pol->prof_tail = 0;
+  }
+  pol->prof_phase = 0;
+  return RG_OK;
+}
+
+int prof_end(rg_policy* pol) {
+  int rc;
+  if (pol->prof)
+    while (pol->prof_tail < pol->prof_head)
+      if ((rc = prof_drain_one(pol))) return rc;
+  return RG_OK;
+}
+
 int copy_weight(rg_policy* pol, void* dst, const void* src, size_t bytes, const char* what) {
   if (!src) return fail(RG_EINVAL, std::string("weights: NULL ") + what);
   HIPTRY(hipMemcpy(dst, src, bytes, hipMemcpyDeviceToDevice));
@@ -602,6 +720,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       {(void**)&pol->row_beg, (size_t)(M * 4)},
       {(void**)&pol->grp_row0, (size_t)(P * 4)},
       {(void**)&pol->grp_row1, (size_t)(P * 4)},
+      {(void**)&pol->coff, (size_t)((S + 1) * 4)},
+      {(void**)&pol->row_tgt, (size_t)(M * 4)},
+      {(void**)&pol->row_out, (size_t)(M * 4)},
+      {(void**)&pol->row_lrow, (size_t)(S * 4)},
       {(void**)&pol->free_stack, (size_t)(pol->pool_pages * 4)},
       {(void**)&pol->state, 64},
       {(void**)&pol->copy_pairs, (size_t)(2 * S * pol->max_pages * 4)},
@@ -645,22 +767,11 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   if (!pol || !prompts || !prompt_len || !G || !tokens || !lengths || !logprobs)
     return fail(RG_EINVAL, "rollout_group: NULL argument");
   hipStream_t st = (hipStream_t)stream;
-  const rg_limits& lim = pol->lim;
-  if (P < 1) return fail(RG_EINVAL, "rollout_group: P < 1");
-  if (max_new < 1) return fail(RG_EINVAL, "rollout_group: max_new < 1");
-  if (P > lim.max_prompts) return fail(RG_ENOMEM, "rollout_group: P exceeds limits.max_prompts");
-  int64_t N = 0, T_pre = 0;
-  int max_plen = 0;
-  for (int p = 0; p < P; ++p) {
-    if (prompt_len[p] < 1) return fail(RG_EINVAL, "rollout_group: prompt_len < 1");
-    if (G[p] < 1) return fail(RG_EINVAL, "rollout_group: G < 1");
-    N += G[p];
-    T_pre += prompt_len[p];
-    max_plen = std::max(max_plen, prompt_len[p]);
-  }
-  if (N > lim.max_seqs) return fail(RG_ENOMEM, "rollout_group: sum(G) exceeds limits.max_seqs");
-  if (T_pre > lim.max_prompt_tokens) return fail(RG_ENOMEM, "rollout_group: prompt tokens exceed limits");
-  if ((int64_t)max_plen + max_new > lim.max_context) return fail(RG_ENOMEM, "rollout_group: context exceeds limits");
+  GroupRun gr;
+  int rc = check_groups(pol, "rollout_group", prompt_len, P, G, max_new, &gr);
+  if (rc) return rc;
+  const int64_t N = gr.N;
+  const int max_plen = gr.max_plen;
   rg_sampling o{};
   o.temperature = 1.f;
   if (opts) o = *opts;
@@ -670,78 +781,13 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
     for (int64_t s = 0; s < N; ++s)
       if (o.forced_len[s] < 1 || o.forced_len[s] > max_new) return fail(RG_EINVAL, "rollout_group: forced_len out of [1, max_new]");
   const int Ni = (int)N;
-  {
-    int64_t pre_pages = 0;
-    for (int p = 0; p < P; ++p) pre_pages += ceil_div(prompt_len[p], pol->page_tok);
-    if (pre_pages > pol->pool_pages) return fail(RG_ENOMEM, "rollout_group: prompt pages exceed the KV pool");
-  }
 
-  // profiling state
-  pol->prof = (o.flags & RG_FLAG_PROFILE) != 0;
-  pol->prof_mask = o.profile_kinds ? o.profile_kinds : 0xFFFFFFFFu;
-  if (pol->prof) {
-    if (pol->prof_ev.empty()) {
-      pol->prof_ev.resize(2 * RG_PROF_RING);
-      pol->prof_kind.resize(RG_PROF_RING);
-      pol->prof_ph.resize(RG_PROF_RING);
-      for (auto& e : pol->prof_ev) HIPTRY(hipEventCreate(&e));
-    }
-    std::memset(pol->kt_ms, 0, sizeof(pol->kt_ms));
-    std::memset(pol->kt_n, 0, sizeof(pol->kt_n));
-    pol->prof_head = pol->prof_tail = 0;
-  }
-  pol->prof_phase = 0;
-
-  // stage host inputs: plen [P], G [P], forced [N]
-  int32_t* hs = pol->h_stage;
-  HIPTRY(hipStreamSynchronize(st));   // the staging buffer may still feed an earlier call's copies
-  std::memcpy(hs, prompt_len, (size_t)P * 4);
-  std::memcpy(hs + P, G, (size_t)P * 4);
-  HIPTRY(hipMemcpyAsync(pol->plen, hs, (size_t)P * 4, hipMemcpyHostToDevice, st));
-  HIPTRY(hipMemcpyAsync(pol->G_dev, hs + P, (size_t)P * 4, hipMemcpyHostToDevice, st));
-  if (o.forced_len) {
-    std::memcpy(hs + 2 * P, o.forced_len, (size_t)N * 4);
-    HIPTRY(hipMemcpyAsync(pol->seq_forced, hs + 2 * P, (size_t)N * 4, hipMemcpyHostToDevice, st));
-  }
+  if ((rc = prof_begin(pol, (o.flags & RG_FLAG_PROFILE) != 0, o.profile_kinds))) return rc;
+  if ((rc = stage_groups(pol, st, gr, prompt_len, G, o.forced_len))) return rc;
   const int32_t* forced_dev = o.forced_len ? pol->seq_forced : nullptr;
-
-  // set-up: offsets, prompt page tables, free stack, output padding
-  SetupArgs sa{};
-  sa.P = P; sa.n_seq = Ni; sa.max_new = max_new; sa.page_tok = pol->page_tok; sa.max_pages = pol->max_pages;
-  sa.pool_pages = pol->pool_pages; sa.plen = pol->plen; sa.prompt_off = pol->prompt_off; sa.grp_off = pol->grp_off;
-  sa.G = pol->G_dev; sa.page_tab = pol->page_tab; sa.free_stack = pol->free_stack; sa.state = pol->state;
-  sa.tokens_out = tokens; sa.logprobs_out = logprobs; sa.last_rows = pol->last_rows;
-  LAUNCH(RG_K_SETUP, launch_setup(sa, st));
-
-  // ---- prefill
-  const int* d_pre = pol->state + 5;
-  LAUNCH(RG_K_SETUP, launch_prefill_rows(pol->prompt_off, P, Ni, pol->row_tab, pol->row_pos, pol->row_beg,
-                                         (int)T_pre, st));
-  LAUNCH(RG_K_EMBED, launch_embed(pol->dtype, pol->w_embed, pol->d, pol->V, prompts, pol->x, pol->state + 7, d_pre,
-                                  (int)T_pre, st));
-  LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
-                                       pol->a_plane, nullptr, d_pre, (int)T_pre, st));
-  int rc = run_layers(pol, st, d_pre, (int)T_pre, max_plen, false, nullptr);
-  if (rc) return rc;
-  rc = run_head(pol, st, pol->state + 6, P, pol->last_rows);
-  if (rc) return rc;
-
-  // ---- fork
-  ForkArgs fa{};
-  fa.P = P; fa.n_seq = Ni; fa.page_tok = pol->page_tok; fa.max_pages = pol->max_pages;
-  fa.share = (o.flags & RG_FLAG_NO_PREFIX_SHARING) ? 0 : 1;
-  fa.grp_off = pol->grp_off; fa.plen = pol->plen; fa.page_tab = pol->page_tab; fa.seq_grp = pol->seq_grp;
-  fa.seq_npages = pol->seq_npages; fa.seq_nshared = pol->seq_nshared; fa.act_seq = pol->act_seq;
-  fa.free_stack = pol->free_stack; fa.state = pol->state; fa.copy_pairs = pol->copy_pairs;
-  LAUNCH(RG_K_SETUP, launch_fork(fa, st));
-  int max_pairs = 0;
-  for (int p = 0; p < P; ++p) {
-    const int n_pref = (int)ceil_div(prompt_len[p], pol->page_tok);
-    const int need = fa.share ? (prompt_len[p] % pol->page_tok ? 1 : 0) : n_pref;
-    max_pairs += need * G[p];
-  }
-  LAUNCH(RG_K_SETUP, launch_page_copy(pol->dtype, pol->kv_pool, pol->geom.page_elems, pol->copy_pairs, max_pairs,
-                                      pol->state, st));
+  if ((rc = prefill_and_fork(pol, st, gr, prompts, prompt_len, G, max_new, !(o.flags & RG_FLAG_NO_PREFIX_SHARING),
+                             tokens, logprobs)))
+    return rc;
 
   // ---- sampling / retirement of one step
   SampleArgs sm{};
@@ -833,11 +879,102 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   if (n_steps == 0) n_steps = last_t + 1;
   const bool bad_token = pol->h_ring[8 * (last_t % RG_RING) + 7] != 0;
   pol->last_steps = n_steps;
-  if (pol->prof)
-    while (pol->prof_tail < pol->prof_head)
-      if ((rc = prof_drain_one(pol))) return rc;
+  if ((rc = prof_end(pol))) return rc;
   if (oom) return fail(RG_ENOMEM, "rollout_group: the KV page pool ran out");
   if (bad_token) return fail(RG_EINVAL, "rollout_group: a prompt or forced token id is outside [0, vocab)");
+  return RG_OK;
+}
+
+int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_len, int32_t P, const int32_t* G,
+                       const int32_t* tokens, const int32_t* lengths, int32_t max_new, float temperature, int32_t flags,
+                       float* logprobs, void* stream) {
+  if (!pol || !prompts || !prompt_len || !G || !tokens || !lengths || !logprobs)
+    return fail(RG_EINVAL, "recompute_logprobs: NULL argument");
+  hipStream_t st = (hipStream_t)stream;
+  GroupRun gr;
+  int rc = check_groups(pol, "recompute_logprobs", prompt_len, P, G, max_new, &gr);
+  if (rc) return rc;
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return fail(RG_EINVAL, "recompute_logprobs: temperature <= 0");
+  if ((int64_t)gr.N * max_new >= INT32_MAX) return fail(RG_EINVAL, "recompute_logprobs: N * max_new >= 2^31");
+  const int N = gr.N;
+  if ((rc = prof_begin(pol, (flags & RG_FLAG_PROFILE) != 0, 0))) return rc;
+  if ((rc = stage_groups(pol, st, gr, prompt_len, G, nullptr))) return rc;
+  if ((rc = prefill_and_fork(pol, st, gr, prompts, prompt_len, G, max_new, !(flags & RG_FLAG_NO_PREFIX_SHARING),
+                             nullptr, logprobs)))
+    return rc;
+
+  // y_0 of every sequence, scored by its prompt's last-position logits
+  pol->prof_phase = 1;
+  LAUNCH(RG_K_SETUP, launch_first_rows(tokens, pol->seq_grp, N, max_new, pol->V, pol->row_lrow, pol->row_tgt,
+                                       pol->row_out, pol->state + 7, st));
+  LAUNCH(RG_K_LOGPROB, launch_token_logprob(pol->logits, pol->V, temperature, pol->row_lrow, pol->row_tgt,
+                                            pol->row_out, logprobs, N, st));
+  // pages for every completion position, and the row offsets
+  ReserveArgs ra{};
+  ra.n_seq = N; ra.max_new = max_new; ra.page_tok = pol->page_tok; ra.max_pages = pol->max_pages;
+  ra.lengths = lengths; ra.plen = pol->plen; ra.seq_grp = pol->seq_grp; ra.seq_npages = pol->seq_npages;
+  ra.page_tab = pol->page_tab; ra.free_stack = pol->free_stack; ra.coff = pol->coff; ra.state = pol->state;
+  LAUNCH(RG_K_SETUP, launch_reserve(ra, st));
+  HIPTRY(hipMemcpyAsync(pol->h_ring, pol->state, 16 * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  HIPTRY(hipStreamSynchronize(st));
+  if (pol->h_ring[2]) return fail(RG_ENOMEM, "recompute_logprobs: the KV page pool ran out");
+  if (pol->h_ring[10]) return fail(RG_EINVAL, "recompute_logprobs: a length is outside [1, max_new]");
+  const int64_t R = pol->h_ring[9];
+
+  // the teacher-forced rows in chunks of m_act; the lm head in slices of the
+  // logits buffer's rows
+  const int chunk = pol->m_act;
+  const int slice = (int)std::max<int64_t>(pol->lim.max_seqs, pol->lim.max_prompts);
+  const int ctx_all = gr.max_plen + max_new;
+  const size_t row_bytes = (size_t)pol->d * pol->eb;
+  int* d_chunk = pol->state + 11;
+  int* d_slice = pol->state + 12;
+  RecomputeRows rr{};
+  rr.n_seq = N; rr.max_new = max_new; rr.V = pol->V; rr.d = pol->d; rr.coff = pol->coff; rr.tokens = tokens;
+  rr.plen = pol->plen; rr.seq_grp = pol->seq_grp; rr.row_tab = pol->row_tab; rr.row_pos = pol->row_pos;
+  rr.row_beg = pol->row_beg; rr.row_tgt = pol->row_tgt; rr.row_out = pol->row_out; rr.x = pol->x;
+  rr.bad_token = pol->state + 7;
+  GemmEpi store{};
+  store.mode = GEMM_EPI_STORE; store.C = pol->logits; store.ldc = pol->V;
+  for (int64_t r0 = 0; r0 < R; r0 += chunk) {
+    const int n = (int)std::min<int64_t>(chunk, R - r0);
+    rr.row0 = (int)r0;
+    LAUNCH(RG_K_EMBED, launch_recompute_rows(pol->dtype, pol->w_embed, rr, n, st));
+    LAUNCH(RG_K_SETUP, launch_fill_i32(d_chunk, 1, n, st));
+    LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
+                                         pol->a_plane, nullptr, d_chunk, n, st));
+    if ((rc = run_layers(pol, st, d_chunk, n, ctx_all, true, nullptr))) return rc;
+    for (int h0 = 0; h0 < n; h0 += slice) {
+      const int m = std::min(slice, n - h0);
+      LAUNCH(RG_K_SETUP, launch_fill_i32(d_slice, 1, m, st));
+      if ((rc = gemm(pol, st, RG_K_GEMM_LM, (const char*)pol->abuf + (size_t)h0 * row_bytes, pol->d, pol->w_lm,
+                     pol->V, d_slice, m, store, false)))
+        return rc;
+      LAUNCH(RG_K_LOGPROB, launch_token_logprob(pol->logits, pol->V, temperature, nullptr, pol->row_tgt + h0,
+                                                pol->row_out + h0, logprobs, m, st));
+    }
+  }
+  HIPTRY(hipMemcpyAsync(pol->h_ring, pol->state, 16 * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  HIPTRY(hipStreamSynchronize(st));
+  if ((rc = prof_end(pol))) return rc;
+  if (pol->h_ring[7]) return fail(RG_EINVAL, "recompute_logprobs: a prompt or completion token id is outside [0, vocab)");
+  return RG_OK;
+}
+
+int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
+                   const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep, double eps_lo,
+                   double eps_hi, int32_t mode, double* out, void* stream) {
+  if (!new_lp || !old_lp || !adv || !lengths || !G || !out) return fail(RG_EINVAL, "grpo_surrogate: NULL argument");
+  if (P < 1 || N < 1 || max_new < 1) return fail(RG_EINVAL, "grpo_surrogate: P, N and max_new must be >= 1");
+  if (!(eps_lo >= 0.0 && eps_lo < 1.0) || !(eps_hi >= 0.0) || !std::isfinite(eps_hi))
+    return fail(RG_EINVAL, "grpo_surrogate: need 0 <= eps_lo < 1 and 0 <= eps_hi");
+  if (mode != RG_LOSS_TOKEN_MEAN && mode != RG_LOSS_SEQ_MEAN) return fail(RG_EINVAL, "grpo_surrogate: unknown mode");
+  SurrogateArgs sa{};
+  sa.new_lp = new_lp; sa.old_lp = old_lp; sa.adv = adv; sa.lengths = lengths; sa.G = G; sa.keep = keep;
+  sa.P = P; sa.N = N; sa.max_new = max_new; sa.mode = mode; sa.eps_lo = eps_lo; sa.eps_hi = eps_hi; sa.out = out;
+  const hipError_t e = launch_surrogate(sa, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("grpo_surrogate launch: ") + hipGetErrorString(e));
   return RG_OK;
 }
 

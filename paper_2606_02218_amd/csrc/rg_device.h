@@ -133,3 +133,51 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   for (int i = 0; i < nw; ++i) r = fmaxf(r, red[i]);
   return r;
 }
+
+// Exclusive prefix sum over the block (blockDim.x multiple of 64, <= 1024);
+// `lds` holds 17 ints.  Returns this thread's exclusive prefix; *total gets
+// the block sum.  Contains barriers: every thread must call it.
+static __device__ int block_excl_scan(int v, int* lds, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) lds[w] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int i = 0; i < nw; ++i) { int tmp = lds[i]; lds[i] = run; run += tmp; }
+    lds[16] = run;
+  }
+  __syncthreads();
+  const int excl = lds[w] + x - v;
+  *total = lds[16];
+  __syncthreads();
+  return excl;
+}
+
+// 1 when every G[p] >= 1 and sum(G) == N, summed in 64 bits so that no
+// choice of G can wrap around to a false match.  Block-wide: every thread of
+// the block calls it and gets the same answer.
+static __device__ bool groups_valid(const int32_t* __restrict__ G, int P, int N) {
+  __shared__ unsigned long long s_sum;
+  __shared__ int s_bad;
+  if (threadIdx.x == 0) { s_sum = 0; s_bad = 0; }
+  __syncthreads();
+  long long loc = 0;
+  int bad = 0;
+  for (int p = threadIdx.x; p < P; p += blockDim.x) {
+    const int g = G[p];
+    bad |= g < 1;
+    loc += g;
+  }
+  if (bad) atomicOr(&s_bad, 1);
+  atomicAdd(&s_sum, (unsigned long long)loc);
+  __syncthreads();
+  const bool ok = !s_bad && s_sum == (unsigned long long)N;
+  __syncthreads();
+  return ok;
+}

@@ -218,3 +218,41 @@ hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P,
 hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,
                                 hipStream_t st);
 hipError_t launch_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* out, hipStream_t st);
+
+// ---- GRPO loss forward (k_loss.hip)
+// After the fork: per-sequence row offsets of the teacher-forced forward
+// (coff [n_seq + 1], prefix of lengths - 1) and the pages its positions need.
+// state[9] = rows in all, state[10] = length out of [1, max_new] seen,
+// state[2] = out of pages.
+struct ReserveArgs {
+  int n_seq, max_new, page_tok, max_pages;
+  const int32_t* lengths; const int32_t* plen; const int32_t* seq_grp;
+  int32_t* seq_npages; int32_t* page_tab; const int32_t* free_stack;
+  int32_t* coff; int32_t* state;
+};
+hipError_t launch_reserve(const ReserveArgs& a, hipStream_t st);
+
+// Rows row0 .. row0 + rows - 1 of the teacher-forced forward: row set-up
+// (row_tab, row_pos, row_beg), embeddings into x, and for each row the token
+// it predicts (row_tgt) and where that token's log-probability goes (row_out).
+struct RecomputeRows {
+  int row0, n_seq, max_new, V, d;
+  const int32_t* coff; const int32_t* tokens; const int32_t* plen; const int32_t* seq_grp;
+  int32_t* row_tab; int32_t* row_pos; int32_t* row_beg; int32_t* row_tgt; int32_t* row_out;
+  float* x; int32_t* bad_token;
+};
+hipError_t launch_recompute_rows(int dtype, const void* embed, const RecomputeRows& a, int rows, hipStream_t st);
+hipError_t launch_first_rows(const int32_t* tokens, const int32_t* seq_grp, int n_seq, int max_new, int V,
+                             int32_t* lrow, int32_t* tgt, int32_t* out, int32_t* bad_token, hipStream_t st);
+// lp[out[r]] = z[tgt[r]]/T - logsumexp(z/T), z = logits row lrow[r] (lrow NULL: r).
+hipError_t launch_token_logprob(const float* logits, int V, float T, const int32_t* lrow, const int32_t* tgt,
+                                const int32_t* out, float* lp, int rows, hipStream_t st);
+
+struct SurrogateArgs {
+  const float* new_lp; const float* old_lp; const float* adv; const int32_t* lengths;
+  const int32_t* G; const int32_t* keep;
+  int P, N, max_new, mode;
+  double eps_lo, eps_hi;
+  double* out;
+};
+hipError_t launch_surrogate(const SurrogateArgs& a, hipStream_t st);

@@ -1,0 +1,238 @@
+"""GPU parity of the GRPO loss forward.
+
+* recompute_logprobs against the oracle's teacher-forced log-probabilities:
+  within 1e-4 for the fp32 tiny model, within 2e-2 (twice the logit
+  tolerance) for bf16 decoders -- a GQA decoder with 6 query heads per kv head
+  and head_dim 128, and a gpt2s-shaped one with ragged prompts.  Limits are
+  chosen so the completion rows run in many chunks and the lm head in many
+  slices, each with a ragged tail.
+* the recompute reproduces the library's own rollout logprobs (same
+  temperature) on a free-running rollout, also at the 1.5B decoder shape,
+  and private prompt pages give bit-identical results.
+* grpo_surrogate against the oracle on seeded inputs: counts exact, loss and
+  clipped fraction within 1e-10 relative, for both aggregation modes, the
+  decoupled clip, keep masks and more than one tile of groups.
+* the whole chain (rollout, advantage, filter, recompute, surrogate) against
+  the oracle's chain on the tiny model.
+* errors: lengths outside [1, max_new], token ids outside the vocabulary, a
+  KV pool too small, invalid G.
+"""
+import numpy as np
+import pytest
+
+from oracle.rollout import rollout as oracle_rollout
+from oracle.grpo import teacher_forced_logprobs, clipped_surrogate
+from oracle.advantage import group_advantage as oracle_adv, zero_variance_filter
+from workload import get_config, make_weights, make_inputs, ModelShape, drifted_logprobs
+from rg_helpers import oracle_for, make_policy, prompts_to_device, LOGIT_TOL
+
+pytestmark = pytest.mark.gpu
+
+GQA = ModelShape(2, 256, 12, 2, 128, 512, 2048, 1e6, dtype="bf16")
+GPT2S = get_config("gpt2s").shape
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available()
+    return torch
+
+
+@pytest.fixture(scope="module")
+def rg():
+    import paper_2606_02218_amd as rg
+    return rg
+
+
+def _np(x):
+    return x.cpu().numpy()
+
+
+def _recompute_case(torch, shape, w, prompts, G, max_new, L, seed, T=1.0, tol=2 * LOGIT_TOL, limits=None):
+    """Oracle rollout (forced lengths) gives the tokens; both sides then score
+    them by teacher forcing."""
+    model = oracle_for(shape, w)
+    ref = oracle_rollout(model, prompts, G, max_new, seed, L, temperature=T)
+    want = teacher_forced_logprobs(model, prompts, G, ref["tokens"], ref["lengths"], T)
+    N = int(np.sum(G))
+    lim = limits or dict(max_seqs=N, max_prompts=len(G), max_prompt_tokens=int(sum(map(len, prompts))),
+                         max_context=max(map(len, prompts)) + max_new)
+    pol = make_policy(shape, w, **lim)
+    tok = torch.from_numpy(ref["tokens"]).cuda()
+    ln = torch.from_numpy(ref["lengths"]).cuda()
+    got = _np(pol.recompute_logprobs(prompts_to_device(prompts), G, tok, ln, temperature=T))
+    valid = np.arange(max_new)[None, :] < ref["lengths"][:, None]
+    assert np.all(got[~valid] == 0)
+    err = float(np.max(np.abs(got[valid] - want[valid])))
+    assert err <= tol, err
+    return pol, ref, got, err
+
+
+def test_recompute_tiny_fp32(torch):
+    wl = get_config("tiny")
+    w = make_weights(wl.shape, 0)
+    rng = np.random.default_rng(21)
+    prompts = [rng.integers(0, wl.shape.vocab - 1, size=n).astype(np.int32) for n in (16, 9, 23)]
+    G = [4, 3, 2]
+    L = rng.integers(1, 33, size=9).astype(np.int32)
+    L[0], L[-1] = 1, 32
+    # max_prompt_tokens 48, max_seqs 9: chunks of 48 rows, lm head slices of 9 rows
+    _, _, _, err = _recompute_case(torch, wl.shape, w, prompts, G, 32, L, 7, T=0.8, tol=1e-4)
+    assert err < 1e-4
+
+
+def test_recompute_gqa_bf16_many_chunks(torch):
+    w = make_weights(GQA, 3)
+    rng = np.random.default_rng(22)
+    prompts = [rng.integers(0, GQA.vocab - 1, size=n).astype(np.int32) for n in (40, 16, 7)]
+    G = [6, 1, 3]
+    L = rng.integers(1, 121, size=10).astype(np.int32)
+    L[0], L[4] = 1, 120
+    # m_act = 63 rows per chunk (about 12 chunks), slices of 10 lm-head rows
+    _recompute_case(torch, GQA, w, prompts, G, 120, L, 11)
+
+
+def test_recompute_gpt2s_ragged_and_sharing(torch):
+    w = make_weights(GPT2S, 0)
+    base = make_inputs(get_config("gpt2s"), 0).prompts
+    prompts = [base[0], base[1][:37], base[2][:100]]
+    G = [8, 5, 3]
+    L = np.random.default_rng(4).integers(1, 41, size=16).astype(np.int32)
+    L[0], L[5] = 1, 40
+    pol, ref, got, _ = _recompute_case(torch, GPT2S, w, prompts, G, 40, L, 1234)
+    got2 = _np(pol.recompute_logprobs(prompts_to_device(prompts), G, torch.from_numpy(ref["tokens"]).cuda(),
+                                      torch.from_numpy(ref["lengths"]).cuda(), share_prefix=False))
+    np.testing.assert_array_equal(got2, got)
+
+
+@pytest.mark.parametrize("name,plen,G,max_new", [("gqa", 33, [4, 4, 2], 64), ("1.5b", 512, [4, 4], 48)])
+def test_recompute_reproduces_rollout_logprobs(torch, name, plen, G, max_new):
+    shape = GQA if name == "gqa" else get_config("1.5b").shape
+    w = make_weights(shape, 5)
+    rng = np.random.default_rng(23)
+    prompts = [rng.integers(0, shape.vocab - 1, size=plen).astype(np.int32) for _ in G]
+    N = sum(G)
+    L = rng.integers(1, max_new + 1, size=N).astype(np.int32)
+    pol = make_policy(shape, w, N, len(G), plen * len(G), plen + max_new)
+    dp = prompts_to_device(prompts)
+    tok, ln, lp = pol.rollout(dp, G, max_new, 99, temperature=0.9, forced_len=L)
+    lp2 = pol.recompute_logprobs(dp, G, tok, ln, temperature=0.9)
+    ln_np = _np(ln)
+    valid = np.arange(max_new)[None, :] < ln_np[:, None]
+    a, b = _np(lp), _np(lp2)
+    assert np.all(b[~valid] == 0)
+    assert float(np.max(np.abs(a[valid] - b[valid]))) <= 2 * LOGIT_TOL
+
+
+def test_recompute_errors(torch, rg):
+    wl = get_config("tiny")
+    w = make_weights(wl.shape, 0)
+    pol = make_policy(wl.shape, w, 8, 2, 32, 48)
+    prompts = prompts_to_device([np.arange(10, dtype=np.int32), np.arange(6, dtype=np.int32)])
+    G = [4, 4]
+    tok = torch.zeros((8, 32), dtype=torch.int32, device="cuda")
+    for bad in (0, 33):
+        ln = torch.full((8,), 5, dtype=torch.int32, device="cuda")
+        ln[3] = bad
+        with pytest.raises(rg.RolloutError, match="length"):
+            pol.recompute_logprobs(prompts, G, tok, ln)
+    ln = torch.full((8,), 5, dtype=torch.int32, device="cuda")
+    tok2 = tok.clone()
+    tok2[6, 2] = wl.shape.vocab
+    with pytest.raises(rg.RolloutError, match="token id"):
+        pol.recompute_logprobs(prompts, G, tok2, ln)
+    tok3 = tok.clone()
+    tok3[6, 7] = -1          # past the length: never read
+    assert np.all(np.isfinite(_np(pol.recompute_logprobs(prompts, G, tok3, ln))))
+    small = make_policy(wl.shape, w, 8, 2, 32, 48, kv_pool_pages=6)
+    ln = torch.full((8,), 30, dtype=torch.int32, device="cuda")
+    with pytest.raises(rg.RolloutError) as e:
+        small.recompute_logprobs(prompts, G, tok, ln)
+    assert e.value.code == -2
+
+
+def _surrogate_inputs(seed, G, T):
+    rng = np.random.default_rng(seed)
+    N = int(np.sum(G))
+    L = rng.integers(1, T + 1, size=N).astype(np.int32)
+    old = rng.normal(-2.0, 1.0, size=(N, T)).astype(np.float32)
+    new = (old + rng.normal(0, 0.25, size=(N, T))).astype(np.float32)
+    adv = rng.normal(size=N).astype(np.float32)
+    return new, old, adv, L
+
+
+@pytest.mark.parametrize("mode", ["token", "seq"])
+@pytest.mark.parametrize("eps", [(0.2, 0.2), (0.2, 0.28)])
+def test_surrogate_parity(torch, rg, mode, eps):
+    rng = np.random.default_rng(31)
+    layouts = [[16] * 32, list(rng.integers(1, 9, size=1500)), [1], [3, 1000, 2]]
+    for k, G in enumerate(layouts):
+        T = 64 if len(G) < 100 else 12
+        new, old, adv, L = _surrogate_inputs(40 + k, G, T)
+        keeps = [None, (rng.random(len(G)) < 0.6).astype(np.int32)]
+        for keep in keeps:
+            want = clipped_surrogate(new, old, adv, L, G, *eps, mode=mode, keep=keep)
+            dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+            got = _np(rg.grpo_surrogate(dev(new), dev(old), dev(adv), dev(L), dev(np.asarray(G, np.int32)), *eps,
+                                        mode=mode, keep=None if keep is None else dev(keep)))
+            assert got[2] == want[2] and got[3] == want[3], (got, want)
+            if want[3] == 0:
+                assert np.all(got == 0)
+                continue
+            assert got[0] == pytest.approx(want[0], rel=1e-10, abs=1e-14)
+            assert got[1] == pytest.approx(want[1], rel=1e-10, abs=1e-14)
+
+
+def test_surrogate_invalid_inputs_give_nan(torch, rg):
+    new, old, adv, L = _surrogate_inputs(50, [4, 4], 8)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    for G in ([4, 3], [4, 0, 4], [2 ** 31 - 1, 2 ** 31 - 1, 10]):
+        got = _np(rg.grpo_surrogate(dev(new), dev(old), dev(adv), dev(L), dev(np.asarray(G, np.int32))))
+        assert np.all(np.isnan(got)), G
+    L2 = L.copy()
+    L2[5] = 9          # beyond max_new = 8
+    got = _np(rg.grpo_surrogate(dev(new), dev(old), dev(adv), dev(L2), dev(np.asarray([4, 4], np.int32))))
+    assert np.all(np.isnan(got))
+    with pytest.raises(rg.RolloutError):
+        rg.grpo_surrogate(dev(new), dev(old), dev(adv), dev(L), dev(np.asarray([4, 4], np.int32)), eps_lo=1.0)
+
+
+def test_loss_chain_matches_oracle_chain(torch, rg):
+    """rollout -> advantage -> filter -> recompute -> surrogate, on both sides
+    from the same seeded inputs (tiny fp32 model)."""
+    wl = get_config("tiny")
+    w = make_weights(wl.shape, 2)
+    rng = np.random.default_rng(24)
+    prompts = [rng.integers(0, wl.shape.vocab - 1, size=16).astype(np.int32) for _ in range(6)]
+    G = [4, 4, 2, 8, 4, 3]
+    N = sum(G)
+    L = rng.integers(1, wl.max_new + 1, size=N).astype(np.int32)
+    rewards = (rng.random(N) < 0.5).astype(np.float32)
+    rewards[:4] = 1.0                       # an all-correct group: dropped by the filter
+    # oracle chain
+    model = oracle_for(wl.shape, w)
+    ref = oracle_rollout(model, prompts, G, wl.max_new, 8, L)
+    old_ref = drifted_logprobs(ref["logprobs"], ref["lengths"], 3, 0.2)
+    adv_ref = oracle_adv(rewards, G, 1e-6, 1)
+    keep_ref, _ = zero_variance_filter(rewards, G)
+    new_ref = teacher_forced_logprobs(model, prompts, G, ref["tokens"], ref["lengths"])
+    want = clipped_surrogate(new_ref, old_ref, adv_ref, ref["lengths"], G, 0.2, 0.28, "token", keep_ref)
+    # library chain
+    pol = make_policy(wl.shape, w, N, len(G), 16 * len(G), 16 + wl.max_new)
+    dp = prompts_to_device(prompts)
+    # the library decodes the oracle's tokens (teacher forcing), so both
+    # chains score the same completions
+    tok = torch.from_numpy(ref["tokens"]).cuda()
+    _, ln, lp = pol.rollout(dp, G, wl.max_new, 8, forced_len=L, force_tokens=tok)
+    np.testing.assert_array_equal(_np(ln), ref["lengths"])
+    old = torch.from_numpy(drifted_logprobs(_np(lp), _np(ln), 3, 0.2)).cuda()
+    r = torch.from_numpy(rewards).cuda()
+    Gd = torch.tensor(G, dtype=torch.int32, device="cuda")
+    adv = rg.group_advantage(r, Gd)
+    keep, _, _ = rg.group_filter(r, Gd)
+    new = pol.recompute_logprobs(dp, G, tok, ln)
+    got = _np(rg.grpo_surrogate(new, old, adv, ln, Gd, 0.2, 0.28, "token", keep))
+    assert _np(keep).tolist() == keep_ref.tolist() and keep_ref[0] == 0
+    assert got[2] == want[2] and got[3] == want[3]
+    assert abs(got[0] - want[0]) < 1e-3, (got, want)
