@@ -164,6 +164,99 @@ def eb_sweep(args):
                       "steps_per_arm": T, "effective_batch": EB, "sizes": list(sizes), "arms": arms}), flush=True)
 
 
+def loss_forward_flops(shape, G, plen, lengths):
+    """Algorithmic flops (one bf16 product per multiply-add pair) of the
+    teacher-forced completion rows, per kernel class: R = sum(L - 1) rows
+    through every projection, the lm head over the R rows, and causal
+    attention of each row over its context (QK^T and PV)."""
+    L, d, F, V = shape.n_layers, shape.d_model, shape.ffn_dim, shape.vocab
+    qd, kvd, hd, nq = shape.q_dim, shape.kv_dim, shape.head_dim, shape.n_q_heads
+    Ls = np.asarray(lengths, np.int64)
+    R = int(np.sum(Ls - 1))
+    # context of the row feeding y_t is plen + t + 1 positions, t = 0 .. L - 2
+    ctx = int(np.sum((Ls - 1) * (plen + 1) + (Ls - 1) * (Ls - 2) // 2))
+    return R, {"gemm_qkv": 2.0 * L * R * (qd + 2 * kvd) * d, "gemm_o": 2.0 * L * R * d * qd,
+               "gemm_gu": 2.0 * L * R * 2 * F * d, "gemm_down": 2.0 * L * R * d * F, "gemm_lm": 2.0 * R * V * d,
+               "attn": 4.0 * L * nq * hd * ctx}
+
+
+def loss_forward(args):
+    """GRPO loss forward on the rollout of the same workload: one step =
+    recompute_logprobs (teacher-forced log-probabilities of every completion
+    token) + grpo_surrogate against a drifted copy of the rollout's
+    logprobs.  Also checks, at full size, that the recompute reproduces the
+    rollout's own logprobs.  Prints one JSON line."""
+    import torch
+    import paper_2606_02218_amd as rg
+    from workload import get_config, make_weights, make_inputs, drifted_logprobs
+
+    wl = get_config(args.workload)
+    shape = wl.shape
+    inp = make_inputs(wl, 0)
+    N = inp.n_seq
+    pol = rg.Policy(shape, make_weights(shape, 0), max_seqs=N, max_prompts=wl.n_prompts,
+                    max_prompt_tokens=wl.n_prompts * wl.prompt_len, max_context=wl.prompt_len + wl.max_new)
+    dev = torch.device("cuda")
+    prompts = torch.from_numpy(inp.prompts).to(dev)
+    G_dev = torch.from_numpy(inp.G).to(dev)
+    rewards = torch.from_numpy(inp.rewards).to(dev)
+    tokens, lengths, lp_roll = pol.rollout(prompts, inp.G, wl.max_new, 1234, forced_len=inp.forced_len)
+    adv = rg.group_advantage(rewards, G_dev, 1e-6, 1)
+    keep, _, _ = rg.group_filter(rewards, G_dev)
+    ln_np = lengths.cpu().numpy()
+    old = torch.from_numpy(drifted_logprobs(lp_roll.cpu().numpy(), ln_np, 0, 0.1)).to(dev)
+    new = torch.empty_like(lp_roll)
+    print("# rollout done", file=sys.stderr, flush=True)
+
+    def step(prof):
+        pol.recompute_logprobs(prompts, inp.G, tokens, lengths, profile=prof, out=new)
+        return rg.grpo_surrogate(new, old, adv, lengths, G_dev, 0.2, 0.28, "token", keep)
+
+    breakdown = {}
+    for i in range(args.warmup):
+        step(i == 0)
+        if i == 0:
+            breakdown = {ph: pol.kernel_times(ph) for ph in (0, 1)}
+        print(f"# warmup step {i} done", file=sys.stderr, flush=True)
+    valid = np.arange(wl.max_new)[None, :] < ln_np[:, None]
+    dev_max = float(np.max(np.abs(new.cpu().numpy()[valid] - lp_roll.cpu().numpy()[valid])))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        out = step(False)
+        print(f"# timed step {i} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    loss = out.cpu().numpy()
+    scored = int(ln_np.sum())
+    ms = dt / args.steps * 1e3
+    res = {"metric": "GRPO loss-forward scored tokens/s (recompute_logprobs + grpo_surrogate)",
+           "value": round(scored / (ms / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 2), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": wl.name, "prompts": wl.n_prompts, "sequences": N, "prompt_len": wl.prompt_len,
+                      "scored_tokens": scored},
+           "surrogate": {"loss": float(loss[0]), "clip_frac": float(loss[1]), "tokens": int(loss[2]),
+                         "sequences": int(loss[3])},
+           "recompute_vs_rollout_logprob_max_abs": round(dev_max, 5)}
+    if breakdown:
+        res["kernel_ms_breakdown"] = {f"{'prefill' if ph == 0 else 'rows'}.{k}": round(v[0], 1)
+                                      for ph in (0, 1) for k, v in sorted(breakdown[ph].items(), key=lambda kv: -kv[1][0])
+                                      if v[1]}
+        R, flops = loss_forward_flops(shape, inp.G, wl.prompt_len, ln_np)
+        rows = breakdown[1]
+        dom = max((k for k in flops if rows[k][1]), key=lambda k: rows[k][0])
+        ms_tot, n = rows[dom]
+        achieved = flops[dom] / (ms_tot / 1e3)
+        res["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(achieved / 1e12, 1),
+                           "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK, 4),
+                           "traffic": None, "avg_launch_us": round(ms_tot / n * 1e3, 2),
+                           "alg_flops_per_launch": round(flops[dom] / n), "launches": n,
+                           "timing": "HIP events around each launch, untimed warmup step"}
+        res["rows_tflops_by_class"] = {k: round(flops[k] / (rows[k][0] / 1e3) / 1e12, 1) for k in flops if rows[k][1]}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -175,6 +268,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eb-sweep", type=int, default=0, metavar="T",
                     help="only run the static-G vs controller sweep at EB = 64 with T steps per arm and exit")
+    ap.add_argument("--loss-forward", action="store_true",
+                    help="only run the GRPO loss forward (logprob recompute + clipped surrogate) and exit")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
     args = ap.parse_args()
@@ -190,6 +285,9 @@ def main():
         return
     if args.eb_sweep:
         eb_sweep(args)
+        return
+    if args.loss_forward:
+        loss_forward(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (groups would shard across GPUs "

@@ -93,6 +93,78 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float
   }
 }
 
+// QKV epilogue straight from the accumulators of one wave (rows
+// m0 + (wm*WM + i)*16 + 4*(lane/16) + e, column tiles wn*WN + j).  One row
+// block i at a time, every load it needs (row position, KV page, the RoPE
+// cos/sin of each rotated pair) is issued before the first store: through
+// restrict-qualified pointers the loads of a block do not wait on the stores
+// of the previous one, so the tile pays a few load latencies instead of one
+// per element.
+template <int WM, int WN>
+__device__ __forceinline__ void qkv_tile_store(const f32x4_t (&acc)[WM][WN], const GemmEpi& ep, int m0, int n0, int M,
+                                               int N, int wm, int wn, int lane,
+                                               const int32_t* __restrict__ row_pos,
+                                               const int32_t* __restrict__ row_tab,
+                                               const int32_t* __restrict__ page_tab,
+                                               const float* __restrict__ rcos, const float* __restrict__ rsin,
+                                               float* __restrict__ q_out, bf16_t* __restrict__ pool) {
+  const int lr = lane & 15;
+  const int hd = ep.hd, half = hd / 2, n_rot = ep.n_q + ep.n_kv;
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+    const int rb = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4;
+    int pos[4];
+    int64_t kvb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = min(rb + e, M - 1);
+      pos[e] = row_pos[r];
+      const int page = page_tab[(int64_t)row_tab[r] * ep.tab_stride + pos[e] / 16];
+      kvb[e] = (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems;
+    }
+    float co[WN / 2][4], si[WN / 2][4];
+#pragma unroll
+    for (int j = 0; j < WN; j += 2) {
+      const int c = min(n0 + (wn * WN + j) * 16 + lr, N - 1);
+      const int p = c % hd, d = (p >> 5) * 16 + (p & 15);
+      const bool rot = c / hd < n_rot;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        co[j / 2][e] = rot ? rcos[(int64_t)pos[e] * half + d] : 1.f;
+        si[j / 2][e] = rot ? rsin[(int64_t)pos[e] * half + d] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < WN; j += 2) {
+      const int c = n0 + (wn * WN + j) * 16 + lr;   // lower tile's column
+      if (c >= N) continue;
+      const int head = c / hd, p = c % hd, d = (p >> 5) * 16 + (p & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (rb + e >= M) continue;
+        const float a = acc[i][j][e], b = acc[i][j + 1][e];
+        const int slot = pos[e] & 15;
+        if (head >= n_rot) {                               // value head: V^T layout, no rotation
+          bf16_t* vb = pool + kvb[e] + ((int64_t)ep.n_kv + head - n_rot) * 16 * hd;
+          vb[kv_v_off(slot, d, hd)] = f32_to_bf16(a);
+          vb[kv_v_off(slot, d + half, hd)] = f32_to_bf16(b);
+          continue;
+        }
+        const float ra = a * co[j / 2][e] - b * si[j / 2][e], rr = b * co[j / 2][e] + a * si[j / 2][e];
+        if (head < ep.n_q) {
+          float* qo = q_out + ((int64_t)(rb + e) * ep.n_q + head) * hd;
+          qo[d] = ra;
+          qo[d + half] = rr;
+        } else {
+          bf16_t* kp = pool + kvb[e] + (int64_t)(head - ep.n_q) * 16 * hd;
+          kp[kv_k_off(slot, d)] = f32_to_bf16(ra);
+          kp[kv_k_off(slot, d + half)] = f32_to_bf16(rr);
+        }
+      }
+    }
+  }
+}
+
 // Epilogue of a finished tile whose split partials are in ep.part: rows
 // m0..m0+BM-1 (< M), columns n0..n0+BN-1 (< N).  Every thread of the block
 // calls it.
@@ -235,8 +307,11 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
           if (r < M) pp[(int64_t)r * N + col] = acc[i][j][e];
         }
       }
-  } else if constexpr (EPI == GEMM_EPI_SWIGLU || EPI == GEMM_EPI_QKV) {
-    // tiles 2m and 2m+1 of a wave pair up: (gate, up) or (dims d, d + half)
+  } else if constexpr (EPI == GEMM_EPI_QKV) {
+    qkv_tile_store<WM, WN>(acc, ep, m0, n0, M, N, wm, wn, lane, ep.row_pos, ep.row_tab, ep.page_tab, ep.rope_cos,
+                           ep.rope_sin, ep.q_out, (bf16_t*)ep.kv_pool);
+  } else if constexpr (EPI == GEMM_EPI_SWIGLU) {
+    // tiles 2m and 2m+1 of a wave pair up: (gate, up)
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -248,10 +323,7 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
           const int r = m0 + (wm * WM + i) * 16 + (lane >> 4) * 4 + e;
           if (r >= M) continue;
           const float a = acc[i][j][e], b = acc[i][j + 1][e];
-          if constexpr (EPI == GEMM_EPI_SWIGLU)
-            act_store<1>(ep.act, (int64_t)r * ep.act_ld + (c >> 5) * 16 + lr, a / (1.0f + expf(-a)) * b);
-          else
-            qkv_store<bf16_t>(ep, r, c, a, b);
+          act_store<1>(ep.act, (int64_t)r * ep.act_ld + (c >> 5) * 16 + lr, a / (1.0f + expf(-a)) * b);
         }
       }
   } else {
