@@ -268,6 +268,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eb-sweep", type=int, default=0, metavar="T",
                     help="only run the static-G vs controller sweep at EB = 64 with T steps per arm and exit")
+    ap.add_argument("--group-prefix", action="store_true",
+                    help="decode steps attend to each prompt's shared prefix once per group (RG_FLAG_GROUP_PREFIX)")
     ap.add_argument("--loss-forward", action="store_true",
                     help="only run the GRPO loss forward (logprob recompute + clipped surrogate) and exit")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
@@ -317,7 +319,7 @@ def main():
 
     def step(i, prof):
         pol.rollout(prompts, inp.G, wl.max_new, 1234 + i, forced_len=inp.forced_len, profile=prof,
-                    out=(tokens, lengths, logprobs))
+                    group_prefix_pass=args.group_prefix, out=(tokens, lengths, logprobs))
         rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)
 
     breakdown, dom = {}, None
@@ -356,7 +358,8 @@ def main():
            "dtype": "bf16", "data": "synthetic",
            "config": {"workload": wl.name, "prompts": wl.n_prompts, "group_size": int(inp.G[0]),
                       "sequences": N, "prompt_len": wl.prompt_len, "max_new": wl.max_new,
-                      "generated_tokens": gen, "decode_steps": int(len(hist_a))},
+                      "generated_tokens": gen, "decode_steps": int(len(hist_a)),
+                      "group_prefix_pass": bool(args.group_prefix)},
            "group_step_s": round(ms_per_step / 1e3, 4)}
     if breakdown:
         res["kernel_ms_breakdown_untimed_step"] = {k: round(v[0], 1) for k, v in

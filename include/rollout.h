@@ -122,6 +122,10 @@ typedef struct rg_policy rg_policy;  /* opaque: packed weights, KV pool, workspa
                                         default: on MI355X the row-by-row pass reads the
                                         shared pages from L2 and is faster at G = 16.     */
 
+#define RG_FLAG_NO_ROW_TILES      8  /* recompute_logprobs: attend row by row instead of by
+                                        tiles of 16 positions of a sequence sharing each
+                                        staged K/V block (a test and measurement aid)     */
+
 /* Sampling options.  A NULL rg_sampling* means temperature 1, natural EOS, no
  * flags.  Token t of sequence s is argmax_v fp32(z_v/T) + g_v where g_v is the
  * fp32 Gumbel variate -log(-log(u)) of the stream documented at
@@ -226,8 +230,9 @@ int group_filter(const float* rewards, const int32_t* G, int32_t P, int32_t N, i
  *   tokens     DEVICE int32 [N*max_new], ids in [0, vocab) for t < lengths[s]
  *   lengths    DEVICE int32 [N], each in [1, max_new]
  *   temperature  > 0 (use the rollout's to reproduce its logprobs)
- *   flags      RG_FLAG_PROFILE and RG_FLAG_NO_PREFIX_SHARING as in
- *              rg_sampling.flags; profiled kernel times land in phase 0
+ *   flags      RG_FLAG_PROFILE, RG_FLAG_NO_PREFIX_SHARING as in
+ *              rg_sampling.flags, RG_FLAG_NO_ROW_TILES; profiled kernel
+ *              times land in phase 0
  *              (prompt prefill) and phase 1 (completion rows)
  *   logprobs   DEVICE fp32 [N*max_new] out; 0 for t >= lengths[s]
  * The KV pool must hold every completion position at once (the default pool

@@ -14,7 +14,7 @@ _lib = None
 
 RG_OK, RG_EINVAL, RG_ENOMEM, RG_EHIP, RG_EUNSUPPORTED = 0, -1, -2, -3, -4
 RG_DTYPE_F32, RG_DTYPE_BF16 = 0, 1
-RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE, RG_FLAG_GROUP_PREFIX = 1, 2, 4
+RG_FLAG_NO_PREFIX_SHARING, RG_FLAG_PROFILE, RG_FLAG_GROUP_PREFIX, RG_FLAG_NO_ROW_TILES = 1, 2, 4, 8
 KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge", "gemm_o", "gemm_gu", "swiglu",
                 "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup", "logprob"]
 
@@ -245,10 +245,12 @@ class Policy:
         return tokens, lengths, logprobs
 
     def recompute_logprobs(self, prompts, G: Sequence[int], tokens, lengths, temperature: float = 1.0,
-                           share_prefix: bool = True, profile: bool = False, out=None, stream=None):
+                           share_prefix: bool = True, row_tiles: bool = True, profile: bool = False, out=None,
+                           stream=None):
         """Teacher-forced log-probabilities [N, max_new] of the completions
         ``tokens`` (device int32 [N, max_new]) with ``lengths`` (device int32
-        [N]) after ``prompts`` (as for ``rollout``)."""
+        [N]) after ``prompts`` (as for ``rollout``).  ``row_tiles=False``
+        attends row by row (RG_FLAG_NO_ROW_TILES)."""
         import torch
         lib = load_library()
         packed, plen = _pack_prompts(prompts)
@@ -260,7 +262,8 @@ class Policy:
         tokens = tokens.to(dtype=torch.int32).contiguous()
         lengths = lengths.to(dtype=torch.int32).contiguous()
         lp = torch.empty((N, max_new), dtype=torch.float32, device=packed.device) if out is None else out
-        flags = (0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+        flags = ((0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
+                 | (0 if row_tiles else RG_FLAG_NO_ROW_TILES))
         plen_a = (C.c_int32 * P)(*plen)
         g_a = (C.c_int32 * P)(*G)
         _check(lib.recompute_logprobs(self._h, _ptr(packed), plen_a, P, g_a, _ptr(tokens), _ptr(lengths), max_new,

@@ -93,7 +93,8 @@ struct rg_policy {
           *act_seq = nullptr, *act_tok = nullptr, *done = nullptr, *row_tab = nullptr, *row_pos = nullptr,
           *free_stack = nullptr, *state = nullptr, *copy_pairs = nullptr, *last_rows = nullptr,
           *hist_active = nullptr, *hist_groups = nullptr, *row_beg = nullptr, *grp_row0 = nullptr,
-          *grp_row1 = nullptr, *coff = nullptr, *row_tgt = nullptr, *row_out = nullptr, *row_lrow = nullptr;
+          *grp_row1 = nullptr, *coff = nullptr, *row_tgt = nullptr, *row_out = nullptr, *row_lrow = nullptr,
+          *tile_r0 = nullptr, *tile_nr = nullptr;
   int64_t* hist_ctx = nullptr;
   int hist_cap = 0;
 
@@ -273,6 +274,13 @@ struct PrefixPass {
   int max_pref;         // largest full-page prefix, (plen / 16) * 16
 };
 
+// Row tiles of prefill-style rows (bf16 models): attention by the row-tile
+// pass instead of the per-row pass.
+struct RowTiles {
+  const int* d_tiles;   // tile count on the device
+  int tiles_ub;         // bound on it, sizes the grid
+};
+
 // The decoder blocks over `rows_ub` rows (actual count at *d_rows), whose
 // row_tab / row_pos / row_beg are set and whose first attention norm is in
 // pol->abuf; ctx_max bounds every row's context length.  pre != NULL runs the
@@ -280,7 +288,7 @@ struct PrefixPass {
 // pol->abuf holds the final norm of every row (final_norm_rows) or x the
 // residual stream after the last block.
 int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, int ctx_max, bool final_norm_rows,
-               const PrefixPass* pre) {
+               const PrefixPass* pre, const RowTiles* tiles = nullptr) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
   // chunks per row: about RG_ATT_TARGET work items (fewer, longer chunks
@@ -301,7 +309,8 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     plan.pre_slots = (int)ceil_div(pre->max_pref, plan.pre_chunk);
     plan.n_slots = plan.pre_slots + n_chunks;
   }
-  if ((int64_t)rows_ub * plan.n_slots > pol->att_rowchunks) return fail(RG_ENOMEM, "attention workspace too small");
+  if (!tiles && (int64_t)rows_ub * plan.n_slots > pol->att_rowchunks)
+    return fail(RG_ENOMEM, "attention workspace too small");
   const float eps = pol->cfg.rms_eps;
   GemmEpi qkv{};
   qkv.mode = GEMM_EPI_QKV;
@@ -319,6 +328,12 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     qkv.layer = l;
     if ((rc = gemm(pol, st, RG_K_GEMM_QKV, pol->abuf, pol->d, pol->w_qkv[l], pol->qkv_n, d_rows, rows_ub, qkv)))
       return rc;
+    if (tiles) {
+      LAUNCH_TIMED(RG_K_ATTN, launch_attention_tile(pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
+                                                    pol->page_tab, tab_stride, pol->row_tab, pol->row_pos,
+                                                    pol->tile_r0, pol->tile_nr, tiles->d_tiles, tiles->tiles_ub,
+                                                    ctx_max, pol->abuf2, pol->a_plane, st));
+    } else {
     if (plan.pre_slots)
       LAUNCH_TIMED(RG_K_ATTN, launch_attention_prefix(pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                                 pol->page_tab, tab_stride, pre->tab_base, pol->plen,
@@ -330,6 +345,7 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     if (plan.n_slots > 1 || pol->dtype != RG_DTYPE_BF16)   // one bf16 slot: the attention wrote abuf2 itself
       LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
                                                 pol->row_beg, plan, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
+    }
     // O projection + residual, then the MLP norm into abuf (fused into the
     // split epilogue when K is split)
     int S;
@@ -724,6 +740,8 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       {(void**)&pol->row_tgt, (size_t)(M * 4)},
       {(void**)&pol->row_out, (size_t)(M * 4)},
       {(void**)&pol->row_lrow, (size_t)(S * 4)},
+      {(void**)&pol->tile_r0, (size_t)((M + S + 1) * 4)},
+      {(void**)&pol->tile_nr, (size_t)((M + S + 1) * 4)},
       {(void**)&pol->free_stack, (size_t)(pol->pool_pages * 4)},
       {(void**)&pol->state, 64},
       {(void**)&pol->copy_pairs, (size_t)(2 * S * pol->max_pages * 4)},
@@ -930,6 +948,11 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
   const size_t row_bytes = (size_t)pol->d * pol->eb;
   int* d_chunk = pol->state + 11;
   int* d_slice = pol->state + 12;
+  int* d_tiles = pol->state + 13;
+  // bf16 models: attention by row tiles (16 positions of a sequence share
+  // each staged K/V block); RG_FLAG_NO_ROW_TILES keeps the per-row pass
+  const bool use_tiles = pol->dtype == RG_DTYPE_BF16 && !(flags & RG_FLAG_NO_ROW_TILES) &&
+                         pol->nq / pol->nkv <= 8 && ctx_all <= 16384;
   RecomputeRows rr{};
   rr.n_seq = N; rr.max_new = max_new; rr.V = pol->V; rr.d = pol->d; rr.coff = pol->coff; rr.tokens = tokens;
   rr.plen = pol->plen; rr.seq_grp = pol->seq_grp; rr.row_tab = pol->row_tab; rr.row_pos = pol->row_pos;
@@ -944,7 +967,10 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
     LAUNCH(RG_K_SETUP, launch_fill_i32(d_chunk, 1, n, st));
     LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
                                          pol->a_plane, nullptr, d_chunk, n, st));
-    if ((rc = run_layers(pol, st, d_chunk, n, ctx_all, true, nullptr))) return rc;
+    RowTiles rt{d_tiles, (int)ceil_div(n, 16) + std::min(n, N)};
+    if (use_tiles) LAUNCH(RG_K_SETUP, launch_row_tiles(pol->row_tab, pol->coff, (int)r0, n, pol->tile_r0,
+                                                       pol->tile_nr, d_tiles, st));
+    if ((rc = run_layers(pol, st, d_chunk, n, ctx_all, true, nullptr, use_tiles ? &rt : nullptr))) return rc;
     for (int h0 = 0; h0 < n; h0 += slice) {
       const int m = std::min(slice, n - h0);
       LAUNCH(RG_K_SETUP, launch_fill_i32(d_slice, 1, m, st));

@@ -458,6 +458,54 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
 }
 
 
+// Staging of one 32-token block of K and V^T through LDS, shared by the
+// prefix and row-tile passes.  The block is 8*HD 16-byte pieces: K pieces
+// (token tk = pc % 32, dims 8*(pc / 32) ..) then V^T pieces (dim pv % HD,
+// tokens 8*(pv / HD) ..); thread tid takes pieces tid + k*nthr.  Every
+// address is formed without branches so that all of a thread's loads are in
+// flight together.  Tokens at or past c1 read token c0 instead (masked).
+template <int HD>
+struct KvStage {
+  static constexpr int KROW = HD + 8;           // LDS row stride of K (elements)
+  static constexpr int VROW = 40;               // LDS row stride of V^T (32 tokens + 8)
+  static constexpr int PIECES = 8 * HD;
+  static constexpr int MAXP = PIECES / 256;     // pieces per thread (at least 4 waves)
+};
+
+template <int HD>
+__device__ __forceinline__ void kv_stage_fetch(u32x4_t (&rg)[KvStage<HD>::MAXP], const bf16_t* __restrict__ pool,
+                                               const KvGeom& g, int64_t koff, int64_t voff, const int* spg, int c0,
+                                               int c1, int t0, int tid, int nthr) {
+#pragma unroll
+  for (int k = 0; k < KvStage<HD>::MAXP; ++k) {
+    int pc = tid + k * nthr;
+    pc = pc < KvStage<HD>::PIECES ? pc : 0;      // spare slots load piece 0 (never stored)
+    const bool isk = pc < 4 * HD;
+    const int pv = pc - 4 * HD;
+    int tok = t0 + (isk ? (pc & 31) : (pv / HD) * 8);
+    tok = tok < c1 ? tok : c0;
+    const int64_t off = isk ? koff + kv_k_off(tok & 15, (pc >> 5) * 8) : voff + kv_v_off(tok & 15, pv % HD, HD);
+    rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + off);
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void kv_stage_stash(const u32x4_t (&rg)[KvStage<HD>::MAXP], bf16_t* sK, bf16_t* sV, int tid,
+                                               int nthr) {
+#pragma unroll
+  for (int k = 0; k < KvStage<HD>::MAXP; ++k) {
+    const int pc = tid + k * nthr;
+    if (pc < KvStage<HD>::PIECES) {
+      const int tk = pc & 31, ck = pc >> 5;
+      const int lrow = 16 * ((tk >> 2) & 1) + (((tk >> 3) << 2) | (tk & 3));   // K rows in fragment lane order
+      const int pv = pc - 4 * HD;
+      bf16_t* dst = pc < 4 * HD ? sK + lrow * KvStage<HD>::KROW + ck * 8
+                                : sV + (pv % HD) * KvStage<HD>::VROW + (pv / HD) * 8;
+      *reinterpret_cast<u32x4_t*>(dst) = rg[k];
+    }
+  }
+}
+
 // Prefix pass.  Workgroup (chunk, kv head, prompt p, row block b) with W
 // waves; wave w scores query rows 16(bW + w) .. +15 of the group (row i =
 // sibling i / rep, GQA head i % rep).
@@ -476,10 +524,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
                                                          const int32_t* __restrict__ grp_row1, int n_rblk,
                                                          AttPlan plan, float* __restrict__ part_o,
                                                          float* __restrict__ part_ml) {
-  constexpr int KROW = HD + 8;                  // LDS row stride of K (elements)
-  constexpr int VROW = 40;                      // LDS row stride of V^T (32 tokens + 8)
-  constexpr int PIECES = 8 * HD;                // 16-byte pieces per block: K 4*HD, V^T 4*HD
-  constexpr int MAXP = PIECES / 256;            // pieces per thread (at least 4 waves)
+  constexpr int KROW = KvStage<HD>::KROW, VROW = KvStage<HD>::VROW;
   __shared__ __attribute__((aligned(16))) bf16_t sK[2][32 * KROW];
   __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VROW];
   __shared__ int spg[64];
@@ -512,44 +557,9 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
   const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
   const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
 
-  u32x4_t rg[MAXP];
-  auto fetch = [&](int t0) {
-#pragma unroll
-    for (int k = 0; k < MAXP; ++k) {
-      const int pc = tid + k * nthr;
-      if (pc < PIECES) {
-        if (pc < 4 * HD) {                       // K: token tk, 8 dims from ck*8 (neighbouring threads: tokens)
-          const int tk = pc & 31, ck = pc >> 5;
-          int tok = t0 + tk;
-          if (tok >= c1) tok = c0;
-          rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff +
-                                                    kv_k_off(tok & 15, ck * 8));
-        } else {                                 // V^T: dim dd, tokens q4*8 .. +7 (neighbouring threads: dims)
-          const int pv = pc - 4 * HD, dd = pv % HD, q4 = pv / HD;
-          int tv = t0 + q4 * 8;
-          if (tv >= c1) tv = c0;
-          rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tv - c0) >> 4] * g.page_elems + voff +
-                                                    kv_v_off(tv & 15, dd, HD));
-        }
-      }
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int k = 0; k < MAXP; ++k) {
-      const int pc = tid + k * nthr;
-      if (pc < PIECES) {
-        if (pc < 4 * HD) {
-          const int tk = pc & 31, ck = pc >> 5;
-          const int lrow = 16 * ((tk >> 2) & 1) + (((tk >> 3) << 2) | (tk & 3));   // fragment lane order
-          *reinterpret_cast<u32x4_t*>(&sK[buf][lrow * KROW + ck * 8]) = rg[k];
-        } else {
-          const int pv = pc - 4 * HD, dd = pv % HD, q4 = pv / HD;
-          *reinterpret_cast<u32x4_t*>(&sV[buf][dd * VROW + q4 * 8]) = rg[k];
-        }
-      }
-    }
-  };
+  u32x4_t rg[KvStage<HD>::MAXP];
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pool, g, koff, voff, spg, c0, c1, t0, tid, nthr); };
+  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, sK[buf], sV[buf], tid, nthr); };
 
   AttState<HD> st;
   st.m = -INFINITY;
@@ -573,6 +583,105 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
                    [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
   }
   if (active && qv) att_store<HD>(st, ((int64_t)row * plan.n_slots + c) * n_q + head, grp, part_o, part_ml);
+}
+
+// Row tiles of one sequence (prefill-style rows: many consecutive positions
+// of a sequence in one launch).  Workgroup (tile, kv head): the tile's rows
+// tile_r0[k] .. +tile_nr[k]-1 hold consecutive positions of one page table
+// row; its nr x rep query rows (row i = tile row i / rep, GQA head i % rep)
+// are scored 16 per wave against each 32-token block of K and V^T, staged
+// once in LDS for all waves (double buffered, as in the prefix pass).  Query
+// row i sees tokens 0 .. row_pos of its row (causal mask per column).  The
+// whole context is one work item, so the normalised output goes straight to
+// the activation planes.
+template <int HD>
+__global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
+    const float* __restrict__ q, int n_q, int n_kv, const bf16_t* __restrict__ pool, KvGeom g, int layer,
+    const int32_t* __restrict__ page_tab, int tab_stride, const int32_t* __restrict__ row_tab,
+    const int32_t* __restrict__ row_pos, const int32_t* __restrict__ tile_r0, const int32_t* __restrict__ tile_nr,
+    const int* __restrict__ d_tiles, ActOut out) {
+  constexpr int KROW = KvStage<HD>::KROW, VROW = KvStage<HD>::VROW;
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][32 * KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VROW];
+  __shared__ int spg[ATT_MAX_CHUNK_PAGES];
+
+  // XCD-aware order: consecutive tiles (one sequence's rows) share an XCD
+  const int64_t b = blockIdx.x;
+  const int64_t per_xcd = (int64_t)gridDim.x / 8;
+  const int64_t w = (b % 8) * per_xcd + b / 8;
+  const int k = (int)(w / n_kv), kvh = (int)(w % n_kv);
+  if (k >= *d_tiles) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nthr = blockDim.x;
+  const int rep = n_q / n_kv;
+  const int r0 = tile_r0[k], nr = tile_nr[k];
+  const int nrows = nr * rep;
+  const int c1 = row_pos[r0 + nr - 1] + 1;      // the tile's last row sees the longest context
+  const int col = lane & 15, grp = lane >> 4;
+  const bool active = wave * 16 < nrows;
+  const int qi = wave * 16 + col;
+  const bool qv = qi < nrows;
+  const int row = r0 + (qv ? qi / rep : 0), head = kvh * rep + (qv ? qi % rep : 0);
+  const int climit = row_pos[row] + 1;
+
+  {
+    const int32_t* tab = page_tab + (int64_t)row_tab[r0] * tab_stride;
+    const int npg = (c1 + 15) >> 4;
+    for (int i = tid; i < npg; i += nthr) spg[i] = tab[i];
+  }
+  bf16x8_t qh[HD / 32], ql[HD / 32];
+  att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
+  __syncthreads();   // page ids
+  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
+
+  u32x4_t rg[KvStage<HD>::MAXP];
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pool, g, koff, voff, spg, 0, c1, t0, tid, nthr); };
+  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, sK[buf], sV[buf], tid, nthr); };
+
+  AttState<HD> st;
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int i = 0; i < HD / 16; ++i) st.o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  fetch(0);
+  int buf = 0;
+  for (int t0 = 0; t0 < c1; t0 += 32, buf ^= 1) {
+    stash(buf);
+    __syncthreads();                             // block t0 in LDS; the other buffer is free
+    if (t0 + 32 < c1) fetch(t0 + 32);
+    if (!active) continue;
+    f32x4_t s[2];
+    const bf16_t* kb0 = &sK[buf][col * KROW + 8 * grp];
+    att_scores<HD>(s, qh, ql, [&](int tt, int kb) {
+      return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kb0 + 16 * tt * KROW + kb * 32));
+    });
+    if (t0 + 32 > climit) {                      // causal mask of this column (token 0 is always visible)
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (t0 + 8 * grp + 4 * tt + j >= climit) s[tt][j] = -INFINITY;
+    }
+    const bf16_t* vb0 = &sV[buf][col * VROW + 8 * grp];
+    att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))),
+                   [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
+  }
+  if (active && qv) {
+    const float inv = 1.0f / st.l;
+    bf16_t* o = (bf16_t*)out.base + ((int64_t)row * n_q + head) * HD + 4 * grp;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      uint32_t h[2], l[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const float v0 = st.o[dt][2 * e] * inv, v1 = st.o[dt][2 * e + 1] * inv;
+        h[e] = pack_bf16x2(v0, v1);
+        l[e] = pack_bf16x2(v0 - __uint_as_float(h[e] << 16), v1 - __uint_as_float(h[e] & 0xFFFF0000u));
+      }
+      *reinterpret_cast<uint2*>(o + dt * 16) = uint2{h[0], h[1]};
+      *reinterpret_cast<uint2*>(o + out.plane + dt * 16) = uint2{l[0], l[1]};
+    }
+  }
 }
 
 template <int SPLIT>
@@ -703,5 +812,28 @@ hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_m
   else
     hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos, row_beg,
                        plan, o, d_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_tile(const float* q, int n_q, int n_kv, int head_dim, const void* kv_pool, KvGeom g,
+                                 int layer, const int32_t* page_tab, int tab_stride, const int32_t* row_tab,
+                                 const int32_t* row_pos, const int32_t* tile_r0, const int32_t* tile_nr,
+                                 const int* d_tiles, int tiles_ub, int max_ctx, void* out, int64_t a_plane,
+                                 hipStream_t st) {
+  if (tiles_ub <= 0) return hipSuccess;
+  const int rep = n_q / n_kv;
+  if (rep * 16 > 16 * ATT_PRE_MAX_WAVES || max_ctx > 16 * ATT_MAX_CHUNK_PAGES) return hipErrorInvalidValue;
+  const int waves = std::max(4, rep);
+  const int64_t items = (int64_t)tiles_ub * n_kv;
+  const unsigned blocks = (unsigned)((items + 7) / 8 * 8);
+  const ActOut o{out, a_plane};
+  if (head_dim == 128)
+    att_launch(k_attention_tile<128>, dim3(blocks), dim3(64 * waves), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g,
+               layer, page_tab, tab_stride, row_tab, row_pos, tile_r0, tile_nr, d_tiles, o);
+  else if (head_dim == 64)
+    att_launch(k_attention_tile<64>, dim3(blocks), dim3(64 * waves), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g,
+               layer, page_tab, tab_stride, row_tab, row_pos, tile_r0, tile_nr, d_tiles, o);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -96,6 +96,37 @@ __global__ __launch_bounds__(256) void k_recompute_rows(RecomputeRows a, const T
   for (int i = threadIdx.x; i < a.d; i += blockDim.x) a.x[(int64_t)r * a.d + i] = ld_f32<T>(e + i);
 }
 
+// Tiles of the chunk's rows for the row-tile attention: each sequence's rows
+// in the chunk, cut into runs of 16 from its first row.  One block of 1024
+// threads; tile k starts at row tile_r0[k] and has tile_nr[k] rows, in row
+// order; *d_tiles gets the count.
+__global__ __launch_bounds__(1024) void k_row_tiles(const int32_t* __restrict__ row_tab,
+                                                    const int32_t* __restrict__ coff, int row0, int n,
+                                                    int32_t* __restrict__ tile_r0, int32_t* __restrict__ tile_nr,
+                                                    int* __restrict__ d_tiles) {
+  __shared__ int lds[17];
+  int carry = 0;
+  for (int base = 0; base < n; base += blockDim.x) {
+    const int r = base + threadIdx.x;
+    int flag = 0, len = 0;
+    if (r < n) {
+      const int s = row_tab[r];
+      const int f = max(coff[s] - row0, 0);         // the sequence's first row in this chunk
+      const int e = min(coff[s + 1] - row0, n);     // one past its last
+      flag = ((r - f) & 15) == 0;
+      len = min(16, e - r);
+    }
+    int tot;
+    const int o = block_excl_scan(flag, lds, &tot) + carry;
+    if (flag) {
+      tile_r0[o] = r;
+      tile_nr[o] = len;
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *d_tiles = carry;
+}
+
 // Step 0 of every sequence: its prompt's last-position logits (row seq_grp[s])
 // score y_0, stored at logprobs[s * max_new].
 __global__ void k_first_rows(const int32_t* __restrict__ tokens, const int32_t* __restrict__ seq_grp, int n_seq,
@@ -252,6 +283,12 @@ hipError_t launch_recompute_rows(int dtype, const void* embed, const RecomputeRo
     hipLaunchKernelGGL(k_recompute_rows<bf16_t>, dim3(rows), dim3(256), 0, st, a, (const bf16_t*)embed);
   else
     hipLaunchKernelGGL(k_recompute_rows<float>, dim3(rows), dim3(256), 0, st, a, (const float*)embed);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row0, int n, int32_t* tile_r0,
+                            int32_t* tile_nr, int* d_tiles, hipStream_t st) {
+  hipLaunchKernelGGL(k_row_tiles, dim3(1), dim3(1024), 0, st, row_tab, coff, row0, n, tile_r0, tile_nr, d_tiles);
   return hipGetLastError();
 }
 

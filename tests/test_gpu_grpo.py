@@ -93,6 +93,23 @@ def test_recompute_gqa_bf16_many_chunks(torch):
     _recompute_case(torch, GQA, w, prompts, G, 120, L, 11)
 
 
+def test_recompute_row_tiles_match_row_pass(torch):
+    """The row-tile attention (16 positions of a sequence per staged K/V
+    block) against the per-row pass: both within the oracle tolerance and
+    within 2e-3 of each other; a long completion spans many tiles and chunks,
+    sequences of length 1 and 2 give empty and one-row tiles."""
+    w = make_weights(GQA, 6)
+    rng = np.random.default_rng(25)
+    prompts = [rng.integers(0, GQA.vocab - 1, size=n).astype(np.int32) for n in (31, 16, 5)]
+    G = [5, 2, 4]
+    L = rng.integers(1, 201, size=11).astype(np.int32)
+    L[0], L[1], L[6], L[-1] = 1, 2, 200, 17
+    pol, ref, got, _ = _recompute_case(torch, GQA, w, prompts, G, 200, L, 13)
+    row = _np(pol.recompute_logprobs(prompts_to_device(prompts), G, torch.from_numpy(ref["tokens"]).cuda(),
+                                     torch.from_numpy(ref["lengths"]).cuda(), row_tiles=False))
+    assert float(np.max(np.abs(row - got))) < 2e-3
+
+
 def test_recompute_gpt2s_ragged_and_sharing(torch):
     w = make_weights(GPT2S, 0)
     base = make_inputs(get_config("gpt2s"), 0).prompts
