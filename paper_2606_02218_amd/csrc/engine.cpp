@@ -222,12 +222,15 @@ struct ProfScope {
 void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits, int* kps) {
   int S = 1;
   if (pol->dtype == RG_DTYPE_BF16) {
-    // Split K only while the output tiles leave the chip short of blocks, and
-    // only as far as the fp32 partials (written once, read once: 8 bytes per
-    // output element and split) stay within twice the weight bytes or 24 MiB.
-    const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub), bn = gemm_tile_cols(pol->dtype, rows_ub);
+    // Split K only while the output tiles leave the chip short of blocks, to
+    // about RG_GEMM_TARGET blocks (twice that for narrow outputs, whose
+    // partials are small), and only as far as the fp32 partials (written
+    // once, read once: 8 bytes per output element and split) stay within
+    // twice the weight bytes or 24 MiB.
+    const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub, N), bn = gemm_tile_cols(pol->dtype, rows_ub);
     const int64_t blocks = ceil_div(N, bn) * ceil_div(rows_ub, bm);
-    if (blocks < RG_GEMM_FULL) S = (int)ceil_div(RG_GEMM_TARGET, blocks);
+    const int64_t target = N >= 8192 ? RG_GEMM_TARGET : 2 * RG_GEMM_TARGET;
+    if (blocks < RG_GEMM_FULL) S = (int)ceil_div(target, blocks);
     const int64_t budget = std::max<int64_t>(4LL * N * K, 24LL << 20);
     S = (int)std::min<int64_t>({(int64_t)S, K / 128, budget / (8LL * rows_ub * N), RG_SPLIT_MAX});
     S = std::max(1, S);

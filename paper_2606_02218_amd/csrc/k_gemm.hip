@@ -478,13 +478,21 @@ hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, c
 
 }  // namespace
 
-int gemm_tile_rows(int dtype, int rows_ub) {
+// Tile rows for a row bound and output width (bf16).  Measured on MI355X over
+// the projection shapes at 32..512 rows: the smallest tiles win while they
+// keep the block count moderate (more, shorter blocks balance the CUs
+// better); wide outputs with many rows take 64-row tiles, and the widest
+// (the lm head) 128-row ones.  The tile shape does not change any result:
+// every output still accumulates K in the same order.
+int gemm_tile_rows(int dtype, int rows_ub, int N) {
   if (dtype != 1) return 16;
+  if (rows_ub > 1024) return 256;
   if (rows_ub <= 16) return 16;
-  if (rows_ub <= 32) return 32;
-  if (rows_ub <= 64) return 64;
-  if (rows_ub <= 1024) return 128;
-  return 256;
+  const int64_t ct = (N + 127) / 128;
+  const int64_t c32 = ct * ((rows_ub + 31) / 32), c64 = ct * ((rows_ub + 63) / 64);
+  if (c64 > 2048) return 128;
+  if (c32 > 2048 || (rows_ub > 128 && c32 > 600)) return 64;
+  return 32;
 }
 
 // Prefill-sized row counts: 256 x 256 tiles of 64 x 128 per wave (twice the
@@ -502,7 +510,7 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
   hipError_t e;
   if (dtype == 1) {
     if (K % BK_MAX || k_per_split % BK_MAX || N % 16) return hipErrorInvalidValue;
-    switch (gemm_tile_rows(dtype, rows_ub)) {
+    switch (gemm_tile_rows(dtype, rows_ub, N)) {
       case 16: e = launch_tiled<16, 128, 1, 2, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 32: e = launch_tiled<32, 128, 1, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 64: e = launch_tiled<64, 128, 2, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;

@@ -41,8 +41,8 @@ bool rg_launch_events_armed();
 // `a_plane`) follow ActOut in rg_device.h: fp32 for fp32 models, hi/lo bf16
 // planes a_plane elements apart for bf16 models.
 
-// Output tile rows / columns launch_gemm uses for a given row bound.
-int gemm_tile_rows(int dtype, int rows_ub);
+// Output tile rows / columns launch_gemm uses for a row bound and width N.
+int gemm_tile_rows(int dtype, int rows_ub, int N);
 int gemm_tile_cols(int dtype, int rows_ub);
 
 // Largest split-K factor of a projection.
