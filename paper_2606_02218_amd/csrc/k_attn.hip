@@ -459,51 +459,83 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
 
 
 // Staging of one 32-token block of K and V^T through LDS, shared by the
-// prefix and row-tile passes.  The block is 8*HD 16-byte pieces: K pieces
-// (token tk = pc % 32, dims 8*(pc / 32) ..) then V^T pieces (dim pv % HD,
-// tokens 8*(pv / HD) ..); thread tid takes pieces tid + k*nthr.  Every
-// address is formed without branches so that all of a thread's loads are in
-// flight together.  Tokens at or past c1 read token c0 instead (masked).
+// prefix and row-tile passes.  The block is 8*HD 16-byte pieces: 4*HD of K
+// (LDS row L = the S^T fragment lane order of its token, 8 dims each) then
+// 4*HD of V^T (dim dd, 8 tokens each); thread tid takes pieces tid + k*nthr.
+// Blocks start on 32-token boundaries of a range that starts on a page, so a
+// piece's page within the block (0 or 1), its offset inside the page and its
+// LDS slot are the same for every block: they are worked out once
+// (KvStagePlan), and a block's fetch is one page-id read and one address add
+// per piece.  Consecutive threads fill consecutive K rows, which keeps the
+// LDS writes free of bank conflicts.  Page ids past the range repeat its
+// last page (KV_STAGE_PAD), so a tail block needs no clamp: its extra tokens
+// are masked by the caller.
 template <int HD>
 struct KvStage {
   static constexpr int KROW = HD + 8;           // LDS row stride of K (elements)
   static constexpr int VROW = 40;               // LDS row stride of V^T (32 tokens + 8)
+  static constexpr int VBASE = 32 * KROW;       // V^T rows follow the K rows in a block buffer
+  static constexpr int BUF = VBASE + HD * VROW; // elements per block buffer
   static constexpr int PIECES = 8 * HD;
   static constexpr int MAXP = PIECES / 256;     // pieces per thread (at least 4 waves)
 };
 
-template <int HD>
-__device__ __forceinline__ void kv_stage_fetch(u32x4_t (&rg)[KvStage<HD>::MAXP], const bf16_t* __restrict__ pool,
-                                               const KvGeom& g, int64_t koff, int64_t voff, const int* spg, int c0,
-                                               int c1, int t0, int tid, int nthr) {
-#pragma unroll
-  for (int k = 0; k < KvStage<HD>::MAXP; ++k) {
-    int pc = tid + k * nthr;
-    pc = pc < KvStage<HD>::PIECES ? pc : 0;      // spare slots load piece 0 (never stored)
-    const bool isk = pc < 4 * HD;
-    const int pv = pc - 4 * HD;
-    int tok = t0 + (isk ? (pc & 31) : (pv / HD) * 8);
-    tok = tok < c1 ? tok : c0;
-    const int64_t off = isk ? koff + kv_k_off(tok & 15, (pc >> 5) * 8) : voff + kv_v_off(tok & 15, pv % HD, HD);
-    rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + off);
-  }
+// Page ids of [c0, c1) (c0 a multiple of 32 from the table start `tab`),
+// padded to whole 32-token blocks with the last page.
+__device__ __forceinline__ void kv_stage_pages(int* spg, const int32_t* __restrict__ tab, int c0, int c1, int tid,
+                                               int nthr) {
+  const int npg = (c1 - c0 + 15) >> 4;
+  const int npad = ((c1 - c0 + 31) >> 5) << 1;
+  for (int i = tid; i < npad; i += nthr) spg[i] = tab[min(i, npg - 1)];
 }
 
 template <int HD>
-__device__ __forceinline__ void kv_stage_stash(const u32x4_t (&rg)[KvStage<HD>::MAXP], bf16_t* sK, bf16_t* sV, int tid,
-                                               int nthr) {
+struct KvStagePlan {
+  int64_t off[KvStage<HD>::MAXP];   // element offset of the piece inside its page
+  int pg[KvStage<HD>::MAXP];        // page of the piece within the block: 0 or 1
+  int dst[KvStage<HD>::MAXP];       // LDS element offset inside a block buffer
+  bool on[KvStage<HD>::MAXP];       // the piece exists
+};
+
+template <int HD>
+__device__ __forceinline__ void kv_stage_plan(KvStagePlan<HD>& pl, int64_t koff, int64_t voff, int tid, int nthr) {
 #pragma unroll
   for (int k = 0; k < KvStage<HD>::MAXP; ++k) {
-    const int pc = tid + k * nthr;
-    if (pc < KvStage<HD>::PIECES) {
-      const int tk = pc & 31, ck = pc >> 5;
-      const int lrow = 16 * ((tk >> 2) & 1) + (((tk >> 3) << 2) | (tk & 3));   // K rows in fragment lane order
-      const int pv = pc - 4 * HD;
-      bf16_t* dst = pc < 4 * HD ? sK + lrow * KvStage<HD>::KROW + ck * 8
-                                : sV + (pv % HD) * KvStage<HD>::VROW + (pv / HD) * 8;
-      *reinterpret_cast<u32x4_t*>(dst) = rg[k];
+    int pc = tid + k * nthr;
+    pl.on[k] = pc < KvStage<HD>::PIECES;
+    pc = pl.on[k] ? pc : 0;                      // spare slots load piece 0 (never stored)
+    if (pc < 4 * HD) {
+      const int L = pc & 31, ck = pc >> 5;
+      const int tk = (((L & 15) >> 2) << 3) | ((L >> 4) << 2) | (L & 3);   // the token whose fragment row is L
+      pl.pg[k] = tk >> 4;
+      pl.off[k] = koff + kv_k_off(tk & 15, ck * 8);
+      pl.dst[k] = L * KvStage<HD>::KROW + ck * 8;
+    } else {
+      const int pv = pc - 4 * HD, dd = pv % HD, q4 = pv / HD;
+      pl.pg[k] = q4 >> 1;
+      pl.off[k] = voff + kv_v_off((q4 * 8) & 15, dd, HD);
+      pl.dst[k] = KvStage<HD>::VBASE + dd * KvStage<HD>::VROW + q4 * 8;
     }
   }
+}
+
+// Pieces of the block starting at token t0 (spg indexes pages from c0).
+template <int HD>
+__device__ __forceinline__ void kv_stage_fetch(u32x4_t (&rg)[KvStage<HD>::MAXP], const KvStagePlan<HD>& pl,
+                                               const bf16_t* __restrict__ pool, int64_t page_elems, const int* spg,
+                                               int c0, int t0) {
+  const int* sp = spg + ((t0 - c0) >> 4);
+#pragma unroll
+  for (int k = 0; k < KvStage<HD>::MAXP; ++k)
+    rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)sp[pl.pg[k]] * page_elems + pl.off[k]);
+}
+
+template <int HD>
+__device__ __forceinline__ void kv_stage_stash(const u32x4_t (&rg)[KvStage<HD>::MAXP], const KvStagePlan<HD>& pl,
+                                               bf16_t* buf) {
+#pragma unroll
+  for (int k = 0; k < KvStage<HD>::MAXP; ++k)
+    if (pl.on[k]) *reinterpret_cast<u32x4_t*>(buf + pl.dst[k]) = rg[k];
 }
 
 // Prefix pass.  Workgroup (chunk, kv head, prompt p, row block b) with W
@@ -525,8 +557,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
                                                          AttPlan plan, float* __restrict__ part_o,
                                                          float* __restrict__ part_ml) {
   constexpr int KROW = KvStage<HD>::KROW, VROW = KvStage<HD>::VROW;
-  __shared__ __attribute__((aligned(16))) bf16_t sK[2][32 * KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VROW];
+  __shared__ __attribute__((aligned(16))) bf16_t sKV[2][KvStage<HD>::BUF];
   __shared__ int spg[64];
 
   const int c = blockIdx.x, kvh = blockIdx.y, p = blockIdx.z / n_rblk, rb = blockIdx.z % n_rblk;
@@ -546,20 +577,18 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
   const bool qv = qi < nrows;
   const int row = r0 + (qv ? qi / rep : 0), head = kvh * rep + (qv ? qi % rep : 0);
 
-  {
-    const int32_t* tab = page_tab + (int64_t)(tab_base + p) * tab_stride + (c0 >> 4);
-    const int npg = (c1 - c0 + 15) >> 4;
-    for (int i = tid; i < npg; i += nthr) spg[i] = tab[i];
-  }
+  kv_stage_pages(spg, page_tab + (int64_t)(tab_base + p) * tab_stride + (c0 >> 4), c0, c1, tid, nthr);
   bf16x8_t qh[HD / 32], ql[HD / 32];
   att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
   __syncthreads();   // page ids
   const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
   const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
 
+  KvStagePlan<HD> pl;
+  kv_stage_plan<HD>(pl, koff, voff, tid, nthr);
   u32x4_t rg[KvStage<HD>::MAXP];
-  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pool, g, koff, voff, spg, c0, c1, t0, tid, nthr); };
-  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, sK[buf], sV[buf], tid, nthr); };
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_elems, spg, c0, t0); };
+  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, pl, sKV[buf]); };
 
   AttState<HD> st;
   st.m = -INFINITY;
@@ -574,11 +603,11 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
     if (t0 + 32 < c1) fetch(t0 + 32);
     if (!active) continue;
     f32x4_t s[2];
-    const bf16_t* kb0 = &sK[buf][col * KROW + 8 * grp];
+    const bf16_t* kb0 = &sKV[buf][col * KROW + 8 * grp];
     att_scores<HD>(s, qh, ql, [&](int tt, int kb) {
       return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kb0 + 16 * tt * KROW + kb * 32));
     });
-    const bf16_t* vb0 = &sV[buf][col * VROW + 8 * grp];
+    const bf16_t* vb0 = &sKV[buf][KvStage<HD>::VBASE + col * VROW + 8 * grp];
     att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))),
                    [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
   }
@@ -601,8 +630,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ tile_r0, const int32_t* __restrict__ tile_nr,
     const int* __restrict__ d_tiles, ActOut out) {
   constexpr int KROW = KvStage<HD>::KROW, VROW = KvStage<HD>::VROW;
-  __shared__ __attribute__((aligned(16))) bf16_t sK[2][32 * KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VROW];
+  __shared__ __attribute__((aligned(16))) bf16_t sKV[2][KvStage<HD>::BUF];
   __shared__ int spg[ATT_MAX_CHUNK_PAGES];
 
   // XCD-aware order: consecutive tiles (one sequence's rows) share an XCD
@@ -623,20 +651,18 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
   const int row = r0 + (qv ? qi / rep : 0), head = kvh * rep + (qv ? qi % rep : 0);
   const int climit = row_pos[row] + 1;
 
-  {
-    const int32_t* tab = page_tab + (int64_t)row_tab[r0] * tab_stride;
-    const int npg = (c1 + 15) >> 4;
-    for (int i = tid; i < npg; i += nthr) spg[i] = tab[i];
-  }
+  kv_stage_pages(spg, page_tab + (int64_t)row_tab[r0] * tab_stride, 0, c1, tid, nthr);
   bf16x8_t qh[HD / 32], ql[HD / 32];
   att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
   __syncthreads();   // page ids
   const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
   const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
 
+  KvStagePlan<HD> pl;
+  kv_stage_plan<HD>(pl, koff, voff, tid, nthr);
   u32x4_t rg[KvStage<HD>::MAXP];
-  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pool, g, koff, voff, spg, 0, c1, t0, tid, nthr); };
-  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, sK[buf], sV[buf], tid, nthr); };
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_elems, spg, 0, t0); };
+  auto stash = [&](int buf) { kv_stage_stash<HD>(rg, pl, sKV[buf]); };
 
   AttState<HD> st;
   st.m = -INFINITY;
@@ -651,7 +677,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
     if (t0 + 32 < c1) fetch(t0 + 32);
     if (!active) continue;
     f32x4_t s[2];
-    const bf16_t* kb0 = &sK[buf][col * KROW + 8 * grp];
+    const bf16_t* kb0 = &sKV[buf][col * KROW + 8 * grp];
     att_scores<HD>(s, qh, ql, [&](int tt, int kb) {
       return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kb0 + 16 * tt * KROW + kb * 32));
     });
@@ -662,7 +688,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
         for (int j = 0; j < 4; ++j)
           if (t0 + 8 * grp + 4 * tt + j >= climit) s[tt][j] = -INFINITY;
     }
-    const bf16_t* vb0 = &sV[buf][col * VROW + 8 * grp];
+    const bf16_t* vb0 = &sKV[buf][KvStage<HD>::VBASE + col * VROW + 8 * grp];
     att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))),
                    [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
   }
