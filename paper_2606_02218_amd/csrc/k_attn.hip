@@ -669,13 +669,13 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
   st.l = 0.f;
 #pragma unroll
   for (int i = 0; i < HD / 16; ++i) st.o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  fetch(0);
-  int buf = 0;
-  for (int t0 = 0; t0 < c1; t0 += 32, buf ^= 1) {
-    stash(buf);
-    __syncthreads();                             // block t0 in LDS; the other buffer is free
-    if (t0 + 32 < c1) fetch(t0 + 32);
-    if (!active) continue;
+  // two register sets in turn keep the next two blocks' loads in flight
+  // while one block is multiplied out of LDS
+  u32x4_t rg2[KvStage<HD>::MAXP];
+  auto fetch2 = [&](int t0) { kv_stage_fetch<HD>(rg2, pl, pool, g.page_elems, spg, 0, t0); };
+  auto stash2 = [&](int buf) { kv_stage_stash<HD>(rg2, pl, sKV[buf]); };
+  auto block = [&](int buf, int t0) {
+    if (!active) return;
     f32x4_t s[2];
     const bf16_t* kb0 = &sKV[buf][col * KROW + 8 * grp];
     att_scores<HD>(s, qh, ql, [&](int tt, int kb) {
@@ -691,6 +691,19 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
     const bf16_t* vb0 = &sKV[buf][KvStage<HD>::VBASE + col * VROW + 8 * grp];
     att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))),
                    [&](int dt) { return *reinterpret_cast<const u32x4_t*>(vb0 + dt * 16 * VROW); });
+  };
+  fetch(0);
+  if (32 < c1) fetch2(32);
+  for (int t0 = 0; t0 < c1; t0 += 64) {
+    stash(0);
+    __syncthreads();                             // block t0 in buffer 0; buffer 1 is free
+    if (t0 + 64 < c1) fetch(t0 + 64);
+    block(0, t0);
+    if (t0 + 32 >= c1) break;
+    stash2(1);
+    __syncthreads();                             // block t0 + 32 in buffer 1; buffer 0 is free
+    if (t0 + 96 < c1) fetch2(t0 + 96);
+    block(1, t0 + 32);
   }
   if (active && qv) {
     const float inv = 1.0f / st.l;
