@@ -1,0 +1,74 @@
+"""Parity at the benchmark's full size: the 1.5B workload exactly as bench.py
+times it (32 prompts x G = 16, 512-token prompts, max_new 4096, forced
+lognormal lengths, seed 1234), checked on outputs the oracle can compute one
+by one and on properties that hold at any size.
+
+* every one of the 512 retired lengths equals its forced length, and every
+  completion has the required structure (EOS last, padding, finite logprobs);
+* prompt 0's 16 siblings over their first three steps: the library's raw
+  logits within 1e-2 (max-abs) of the fp64 oracle's, and its tokens equal to
+  the oracle's free-running ones except where the oracle's top-2 margin is
+  below 1e-2;
+* the teacher-forced recompute reproduces the rollout's log-probabilities
+  over all 770,996 completion tokens (within 2e-2).
+"""
+import numpy as np
+import pytest
+
+from oracle.rollout import rollout as oracle_rollout
+from workload import get_config, make_weights, make_inputs
+from rg_helpers import oracle_for, check_structure, MARGIN_TOL, LOGIT_TOL
+
+pytestmark = pytest.mark.gpu
+
+STEPS = 3
+
+
+@pytest.mark.timeout(400)
+def test_full_1p5b_workload_sampled_against_oracle():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2606_02218_amd as rg
+    wl = get_config("1.5b")
+    shape = wl.shape
+    w = make_weights(shape, 0)
+    inp = make_inputs(wl, 0)
+    N = inp.n_seq
+    print(f"full-size case: workload {wl.name}, N={N}, max_new={wl.max_new}, seed 1234", flush=True)
+    pol = rg.Policy(shape, w, max_seqs=N, max_prompts=wl.n_prompts, max_prompt_tokens=wl.n_prompts * wl.prompt_len,
+                    max_context=wl.prompt_len + wl.max_new)
+    prompts = torch.from_numpy(inp.prompts).cuda()
+    tok, ln, lp, dump = pol.rollout(prompts, inp.G, wl.max_new, 1234, forced_len=inp.forced_len, dump_steps=STEPS)
+    torch.cuda.synchronize()
+    tok_np, ln_np, lp_np = tok.cpu().numpy(), ln.cpu().numpy(), lp.cpu().numpy()
+    np.testing.assert_array_equal(ln_np, inp.forced_len)
+    check_structure(tok_np, ln_np, lp_np, shape.eos_id, wl.max_new, inp.forced_len)
+
+    # full-size property: the recompute reproduces the rollout's logprobs
+    lp2 = pol.recompute_logprobs(prompts, inp.G, tok, ln).cpu().numpy()
+    valid = np.arange(wl.max_new)[None, :] < ln_np[:, None]
+    assert np.all(lp2[~valid] == 0)
+    assert float(np.max(np.abs(lp2[valid] - lp_np[valid]))) <= 2 * LOGIT_TOL
+    del lp2
+
+    # sampled outputs: prompt 0's siblings, first STEPS steps, against the oracle
+    g0 = int(inp.G[0])
+    dump0 = dump[:, :g0].cpu().numpy().astype(np.float64)
+    del dump
+    pol.close()
+    torch.cuda.empty_cache()
+    print("oracle: prefill of prompt 0 and its siblings' first steps", flush=True)
+    ref = oracle_rollout(oracle_for(shape, w), inp.prompts, inp.G, wl.max_new, 1234, inp.forced_len,
+                         max_steps=STEPS, prompt_subset=[0], record_steps=STEPS)
+    worst, split = 0.0, 0
+    for s in range(g0):
+        for t in range(min(STEPS, int(inp.forced_len[s]))):
+            worst = max(worst, float(np.max(np.abs(dump0[t, s] - ref["logits"][(s, t)]))))
+            if tok_np[s, t] != ref["tokens"][s, t]:
+                assert ref["margins"][s, t] < MARGIN_TOL, (s, t, ref["margins"][s, t])
+                split += 1
+                break
+            assert abs(lp_np[s, t] - ref["logprobs"][s, t]) <= 2 * LOGIT_TOL
+    print(f"worst logit gap {worst:.2e} over prompt 0's siblings, {split} split at a low margin", flush=True)
+    assert worst <= LOGIT_TOL, worst
+    assert split <= 2, split
