@@ -533,7 +533,7 @@ int prefill_and_fork(rg_policy* pol, hipStream_t st, const GroupRun& gr, const i
     const int need = share ? (prompt_len[p] % pol->page_tok ? 1 : 0) : n_pref;
     max_pairs += need * G[p];
   }
-  LAUNCH(RG_K_SETUP, launch_page_copy(pol->dtype, pol->kv_pool, pol->geom.page_elems, pol->copy_pairs, max_pairs,
+  LAUNCH(RG_K_SETUP, launch_page_copy(pol->dtype, pol->kv_pool, pol->geom, pol->copy_pairs, max_pairs,
                                       pol->state, st));
   return RG_OK;
 }
@@ -614,8 +614,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   pol->m_act = std::max(lim.max_prompt_tokens, lim.max_seqs);
   KvGeom& g = pol->geom;
   g.page_tok = pol->page_tok; g.n_layers = pol->L; g.n_kv = pol->nkv; g.head_dim = pol->hd;
-  g.layer_elems = 2LL * pol->nkv * pol->page_tok * pol->hd;
-  g.page_elems = g.layer_elems * pol->L;
+  g.slab_elems = 2LL * pol->nkv * pol->page_tok * pol->hd;
   const size_t eb = pol->eb;
   const int64_t d = pol->d;
   int rc;
@@ -699,7 +698,9 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
     pol->pool_pages = ceil_div(lim.max_prompt_tokens, pol->page_tok) + lim.max_prompts +
                       (int64_t)lim.max_seqs * (ceil_div(lim.max_context, pol->page_tok) + 1);
   if (pol->pool_pages > INT32_MAX) return bail(fail(RG_ENOMEM, "KV pool exceeds 2^31 pages"));
-  if ((rc = pol->alloc(&pol->kv_pool, (size_t)pol->pool_pages * g.page_elems * eb))) return bail(rc);
+  g.page_stride = g.slab_elems;                      // layer-major pool
+  g.layer_stride = g.slab_elems * pol->pool_pages;
+  if ((rc = pol->alloc(&pol->kv_pool, (size_t)pol->pool_pages * g.slab_elems * pol->L * eb))) return bail(rc);
 
   // ---- workspace
   const int64_t M = pol->m_act, S = lim.max_seqs, P = lim.max_prompts;

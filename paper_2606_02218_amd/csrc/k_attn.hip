@@ -25,6 +25,7 @@
 // while the current block is multiplied.
 // fp32 KV (fp32 models): a plain per-token VALU kernel.
 #include <algorithm>
+#include <cstdlib>
 
 #include "rg_device.h"
 #include "rg_kernels.h"
@@ -89,8 +90,8 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     sq[i] = q[((int64_t)r * n_q + kvh * rep) * hd + i];
   if (tid < rep) { s_m[tid] = -INFINITY; s_l[tid] = 0.f; }
   const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * hd;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * hd;
+  const int64_t koff = (int64_t)layer * g.layer_stride + (int64_t)kvh * 16 * hd;
+  const int64_t voff = (int64_t)layer * g.layer_stride + ((int64_t)n_kv + kvh) * 16 * hd;
 
   // each thread owns output slots (h, d) = idx / hd, idx % hd for idx = tid + 256*k
   const int n_own = (rep * hd + 255) / 256;
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
     // ---- scores: one token per thread
     if (tid < nt) {
       const int j = t0 + tid;
-      const KV* kp = pool + (int64_t)tab[j >> 4] * g.page_elems + koff;
+      const KV* kp = pool + (int64_t)tab[j >> 4] * g.page_stride + koff;
       float dot[ATT_MAX_REP];
 #pragma unroll
       for (int h = 0; h < ATT_MAX_REP; ++h) dot[h] = 0.f;
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
         float a = acc[k] * s_alpha[h];
         for (int jj = 0; jj < nt; ++jj) {
           const int j = t0 + jj;
-          const KV* vp = pool + (int64_t)tab[j >> 4] * g.page_elems + voff;
+          const KV* vp = pool + (int64_t)tab[j >> 4] * g.page_stride + voff;
           a = fmaf(sp[h * ATT_TILE + jj], ld_f32<KV>(vp + kv_v_off(j & 15, d, hd)), a);
         }
         acc[k] = a;
@@ -338,19 +339,19 @@ __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restri
   for (int tt = 0; tt < 2; ++tt) {
     int tok = t0 + 8 * (col >> 2) + 4 * tt + (col & 3);
     if (tok >= c1) tok = c0;
-    const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_elems + koff + kv_k_off(tok & 15, 8 * grp);
+    const bf16_t* kp = pool + (int64_t)spg[(tok - c0) >> 4] * g.page_stride + koff + kv_k_off(tok & 15, 8 * grp);
 #pragma unroll
     for (int kb = 0; kb < HD / 32; ++kb) b.k[tt][kb] = *reinterpret_cast<const u32x4_t*>(kp + kb * 4 * 128);
   }
   const int tv = t0 + 8 * grp;
   const int pg = spg[((tv < c1 ? tv : c0) - c0) >> 4];
-  const bf16_t* vp = pool + (int64_t)pg * g.page_elems + voff + kv_v_off(tv & 15, col, HD);
+  const bf16_t* vp = pool + (int64_t)pg * g.page_stride + voff + kv_v_off(tv & 15, col, HD);
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) b.v[dt] = *reinterpret_cast<const u32x4_t*>(vp + dt * 16 * 8);
 }
 
-template <int HD>
-__global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
+template <int HD, int NB>
+__global__ __launch_bounds__(64, NB > 2 ? 1 : 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
                                                        const bf16_t* __restrict__ pool, KvGeom g, int layer,
                                                        const int32_t* __restrict__ page_tab, int tab_stride,
                                                        const int32_t* __restrict__ row_tab,
@@ -390,10 +391,13 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
     for (int i = lane; i < npg; i += 64) spg[i] = tab[i];
     __syncthreads();
   }
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
-  AttBlock<HD> ba, bb;
-  att_load<HD>(ba, pool, g, koff, voff, spg, c0, c1, c0, col, grp);   // first block in flight during the q set-up
+  const int64_t koff = (int64_t)layer * g.layer_stride + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_stride + ((int64_t)n_kv + kvh) * 16 * HD;
+  // NB register blocks in a ring: the next NB-1 blocks' loads are in flight
+  // while one block is multiplied out (a launch holds about one wave per
+  // SIMD, so latency is hidden inside the wave)
+  AttBlock<HD> bk[NB];
+  att_load<HD>(bk[0], pool, g, koff, voff, spg, c0, c1, c0, col, grp);   // first block in flight during the q set-up
   // Q^T fragments (lanes >= rep: zero padding columns), parked in LDS in lane
   // order so that each lane reads back its own 16-byte pieces
   __shared__ __attribute__((aligned(16))) u32x4_t sq[2][HD / 32][64];
@@ -427,12 +431,23 @@ __global__ __launch_bounds__(64, 2) void k_attention_mfma(const float* __restric
     att_scores<HD>(s, qh, ql, [&](int tt, int kb) { return __builtin_bit_cast(bf16x8_t, blk.k[tt][kb]); });
     att_update<HD>(st, s, t0 + 32 > c1, min(8, max(0, c1 - (t0 + 8 * grp))), [&](int dt) { return blk.v[dt]; });
   };
-  for (int t0 = c0; t0 < c1; t0 += 64) {
-    if (t0 + 32 < c1) att_load<HD>(bb, pool, g, koff, voff, spg, c0, c1, t0 + 32, col, grp);
-    step(ba, t0);
-    if (t0 + 32 >= c1) break;
-    if (t0 + 64 < c1) att_load<HD>(ba, pool, g, koff, voff, spg, c0, c1, t0 + 64, col, grp);
-    step(bb, t0 + 32);
+#pragma unroll
+  for (int j = 1; j < NB - 1; ++j)
+    if (c0 + 32 * j < c1) att_load<HD>(bk[j], pool, g, koff, voff, spg, c0, c1, c0 + 32 * j, col, grp);
+  for (int t0 = c0; t0 < c1; t0 += 32 * NB) {
+    bool done = false;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int tb = t0 + 32 * j;
+      if (!done && tb < c1) {
+        const int tn = tb + 32 * (NB - 1);
+        if (tn < c1) att_load<HD>(bk[(j + NB - 1) % NB], pool, g, koff, voff, spg, c0, c1, tn, col, grp);
+        step(bk[j], tb);
+      } else {
+        done = true;
+      }
+    }
+    if (done) break;
   }
   if (col < rep) {
     if (plan.n_slots == 1) {   // the whole context in one work item: normalise and write the activation
@@ -522,12 +537,12 @@ __device__ __forceinline__ void kv_stage_plan(KvStagePlan<HD>& pl, int64_t koff,
 // Pieces of the block starting at token t0 (spg indexes pages from c0).
 template <int HD>
 __device__ __forceinline__ void kv_stage_fetch(u32x4_t (&rg)[KvStage<HD>::MAXP], const KvStagePlan<HD>& pl,
-                                               const bf16_t* __restrict__ pool, int64_t page_elems, const int* spg,
+                                               const bf16_t* __restrict__ pool, int64_t page_stride, const int* spg,
                                                int c0, int t0) {
   const int* sp = spg + ((t0 - c0) >> 4);
 #pragma unroll
   for (int k = 0; k < KvStage<HD>::MAXP; ++k)
-    rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)sp[pl.pg[k]] * page_elems + pl.off[k]);
+    rg[k] = *reinterpret_cast<const u32x4_t*>(pool + (int64_t)sp[pl.pg[k]] * page_stride + pl.off[k]);
 }
 
 template <int HD>
@@ -581,13 +596,13 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
   bf16x8_t qh[HD / 32], ql[HD / 32];
   att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
   __syncthreads();   // page ids
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
+  const int64_t koff = (int64_t)layer * g.layer_stride + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_stride + ((int64_t)n_kv + kvh) * 16 * HD;
 
   KvStagePlan<HD> pl;
   kv_stage_plan<HD>(pl, koff, voff, tid, nthr);
   u32x4_t rg[KvStage<HD>::MAXP];
-  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_elems, spg, c0, t0); };
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_stride, spg, c0, t0); };
   auto stash = [&](int buf) { kv_stage_stash<HD>(rg, pl, sKV[buf]); };
 
   AttState<HD> st;
@@ -655,13 +670,13 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
   bf16x8_t qh[HD / 32], ql[HD / 32];
   att_load_q<HD>(q + ((int64_t)row * n_q + head) * HD, qv, grp, qh, ql);
   __syncthreads();   // page ids
-  const int64_t koff = (int64_t)layer * g.layer_elems + (int64_t)kvh * 16 * HD;
-  const int64_t voff = (int64_t)layer * g.layer_elems + ((int64_t)n_kv + kvh) * 16 * HD;
+  const int64_t koff = (int64_t)layer * g.layer_stride + (int64_t)kvh * 16 * HD;
+  const int64_t voff = (int64_t)layer * g.layer_stride + ((int64_t)n_kv + kvh) * 16 * HD;
 
   KvStagePlan<HD> pl;
   kv_stage_plan<HD>(pl, koff, voff, tid, nthr);
   u32x4_t rg[KvStage<HD>::MAXP];
-  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_elems, spg, 0, t0); };
+  auto fetch = [&](int t0) { kv_stage_fetch<HD>(rg, pl, pool, g.page_stride, spg, 0, t0); };
   auto stash = [&](int buf) { kv_stage_stash<HD>(rg, pl, sKV[buf]); };
 
   AttState<HD> st;
@@ -672,7 +687,7 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
   // two register sets in turn keep the next two blocks' loads in flight
   // while one block is multiplied out of LDS
   u32x4_t rg2[KvStage<HD>::MAXP];
-  auto fetch2 = [&](int t0) { kv_stage_fetch<HD>(rg2, pl, pool, g.page_elems, spg, 0, t0); };
+  auto fetch2 = [&](int t0) { kv_stage_fetch<HD>(rg2, pl, pool, g.page_stride, spg, 0, t0); };
   auto stash2 = [&](int buf) { kv_stage_stash<HD>(rg2, pl, sKV[buf]); };
   auto block = [&](int buf, int t0) {
     if (!active) return;
@@ -795,8 +810,9 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
 #define RG_ATT_MFMA(HD)                                                                                          \
-    att_launch(k_attention_mfma<HD>, grid1, dim3(64), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, page_tab, \
-               tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, ActOut{out, a_plane}, d_rows)
+    att_launch(k_attention_mfma<HD, 2>, grid1, dim3(64), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer,     \
+               page_tab, tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, ActOut{out, a_plane}, \
+               d_rows)
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;

@@ -71,7 +71,7 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float
   if (head >= ep.n_q + ep.n_kv) {                     // value head: no rotation, V^T layout
     const int kvh = head - ep.n_q - ep.n_kv;
     const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
-    KV* vb = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
+    KV* vb = pool + (int64_t)page * ep.geom.page_stride + (int64_t)ep.layer * ep.geom.layer_stride +
              ((int64_t)ep.n_kv + kvh) * 16 * hd;
     kv_store<KV>(vb + kv_v_off(pos & 15, d, hd), a);
     kv_store<KV>(vb + kv_v_off(pos & 15, d + half, hd), b);
@@ -86,7 +86,7 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& ep, int r, int c, float
   } else {
     const int kvh = head - ep.n_q;
     const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
-    KV* kp = pool + (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems +
+    KV* kp = pool + (int64_t)page * ep.geom.page_stride + (int64_t)ep.layer * ep.geom.layer_stride +
              (int64_t)kvh * 16 * hd;
     kv_store<KV>(kp + kv_k_off(pos & 15, d), ra);
     kv_store<KV>(kp + kv_k_off(pos & 15, d + half), rb);
@@ -120,7 +120,7 @@ __device__ __forceinline__ void qkv_tile_store(const f32x4_t (&acc)[WM][WN], con
       const int r = min(rb + e, M - 1);
       pos[e] = row_pos[r];
       const int page = page_tab[(int64_t)row_tab[r] * ep.tab_stride + pos[e] / 16];
-      kvb[e] = (int64_t)page * ep.geom.page_elems + (int64_t)ep.layer * ep.geom.layer_elems;
+      kvb[e] = (int64_t)page * ep.geom.page_stride + (int64_t)ep.layer * ep.geom.layer_stride;
     }
     float co[WN / 2][4], si[WN / 2][4];
 #pragma unroll

@@ -68,15 +68,19 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, co
   for (int i = threadIdx.x; i < d; i += blockDim.x) act_store<SPLIT>(out, (int64_t)r * d + i, xr[i] * inv * g[i]);
 }
 
+// Copy-on-write of whole pages: every layer's slab of page pairs[2k] to page
+// pairs[2k+1], for k < state[3].
 template <typename KV>
-__global__ void k_page_copy(KV* __restrict__ pool, int64_t page_elems, const int32_t* __restrict__ pairs,
+__global__ void k_page_copy(KV* __restrict__ pool, KvGeom g, const int32_t* __restrict__ pairs,
                             const int32_t* __restrict__ state) {
   const int k = blockIdx.y;
   if (k >= state[3]) return;
-  const KV* src = pool + (int64_t)pairs[2 * k] * page_elems;
-  KV* dst = pool + (int64_t)pairs[2 * k + 1] * page_elems;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < page_elems; i += (int64_t)gridDim.x * blockDim.x)
-    dst[i] = src[i];
+  const int64_t src = (int64_t)pairs[2 * k] * g.page_stride, dst = (int64_t)pairs[2 * k + 1] * g.page_stride;
+  const int64_t n = g.slab_elems * g.n_layers;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t l = i / g.slab_elems, j = i - l * g.slab_elems;
+    pool[dst + l * g.layer_stride + j] = pool[src + l * g.layer_stride + j];
+  }
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t n, int32_t v) {
@@ -156,14 +160,14 @@ hipError_t launch_rmsnorm(int dtype, const float* x, const float* g, int d, floa
   return hipGetLastError();
 }
 
-hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs, int max_pairs,
+hipError_t launch_page_copy(int dtype, void* kv_pool, const KvGeom& g, const int32_t* copy_pairs, int max_pairs,
                             const int32_t* state, hipStream_t st) {
   if (max_pairs <= 0) return hipSuccess;
   dim3 grid(64, max_pairs);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_page_copy<bf16_t>, grid, dim3(256), 0, st, (bf16_t*)kv_pool, page_elems, copy_pairs, state);
+    hipLaunchKernelGGL(k_page_copy<bf16_t>, grid, dim3(256), 0, st, (bf16_t*)kv_pool, g, copy_pairs, state);
   else
-    hipLaunchKernelGGL(k_page_copy<float>, grid, dim3(256), 0, st, (float*)kv_pool, page_elems, copy_pairs, state);
+    hipLaunchKernelGGL(k_page_copy<float>, grid, dim3(256), 0, st, (float*)kv_pool, g, copy_pairs, state);
   return hipGetLastError();
 }
 

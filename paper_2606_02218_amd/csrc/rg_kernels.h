@@ -9,16 +9,20 @@
 #include "rg_device.h"
 
 struct KvGeom {
-  int page_tok;        // tokens per page (16)
+  int page_tok;         // tokens per page (16)
   int n_layers, n_kv, head_dim;
-  int64_t page_elems;  // elements of one page across all layers
-  int64_t layer_elems; // elements of one layer inside a page: 2 * n_kv * page_tok * head_dim
+  int64_t slab_elems;   // elements of one page in one layer: 2 * n_kv * page_tok * head_dim
+  int64_t page_stride;  // elements from page p to page p + 1 within a layer
+  int64_t layer_stride; // elements from layer l to layer l + 1 within a page
 };
 
-// Inside a page, layer l holds a key slab per kv head h at
-//   page*page_elems + l*layer_elems + h*16*head_dim
+// Layer l of page p holds a key slab per kv head h at
+//   p*page_stride + l*layer_stride + h*16*head_dim
 // and a value slab at
-//   page*page_elems + l*layer_elems + (n_kv + h)*16*head_dim.
+//   p*page_stride + l*layer_stride + (n_kv + h)*16*head_dim.
+// The pool is layer-major (page_stride = slab_elems, layer_stride =
+// pool_pages * slab_elems): one layer's pages are contiguous, so a layer's
+// attention pass touches 1/n_layers of the pool's address range.
 // Both slabs are made of 16-byte granules of 8 elements (bf16): keys as
 // [d/8][slot][8] (8 consecutive dims of one token), values as [slot/8][d][8]
 // (8 consecutive tokens of one dim).  A quarter-wave of lanes reading the
@@ -196,7 +200,7 @@ struct ForkArgs {
   int32_t* copy_pairs;      // out: [2*k] (src page, dst page); count in state[3]
 };
 hipError_t launch_fork(const ForkArgs& a, hipStream_t st);
-hipError_t launch_page_copy(int dtype, void* kv_pool, int64_t page_elems, const int32_t* copy_pairs,
+hipError_t launch_page_copy(int dtype, void* kv_pool, const KvGeom& g, const int32_t* copy_pairs,
                             int max_pairs, const int32_t* state, hipStream_t st);
 
 // Rollout set-up: prompt tables, free stack, output padding, counters.
