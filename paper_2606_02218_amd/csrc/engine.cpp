@@ -957,6 +957,7 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
   // each staged K/V block); RG_FLAG_NO_ROW_TILES keeps the per-row pass
   const bool use_tiles = pol->dtype == RG_DTYPE_BF16 && !(flags & RG_FLAG_NO_ROW_TILES) &&
                          pol->nq / pol->nkv <= 8 && ctx_all <= 16384;
+  const int tile_rows = att_tile_rows(pol->nq, pol->nkv);
   RecomputeRows rr{};
   rr.n_seq = N; rr.max_new = max_new; rr.V = pol->V; rr.d = pol->d; rr.coff = pol->coff; rr.tokens = tokens;
   rr.plen = pol->plen; rr.seq_grp = pol->seq_grp; rr.row_tab = pol->row_tab; rr.row_pos = pol->row_pos;
@@ -971,8 +972,8 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
     LAUNCH(RG_K_SETUP, launch_fill_i32(d_chunk, 1, n, st));
     LAUNCH(RG_K_RMSNORM, launch_rmsnorm(pol->dtype, pol->x, pol->g_attn[0], pol->d, pol->cfg.rms_eps, pol->abuf,
                                          pol->a_plane, nullptr, d_chunk, n, st));
-    RowTiles rt{d_tiles, (int)ceil_div(n, 16) + std::min(n, N)};
-    if (use_tiles) LAUNCH(RG_K_SETUP, launch_row_tiles(pol->row_tab, pol->coff, (int)r0, n, pol->tile_r0,
+    RowTiles rt{d_tiles, (int)ceil_div(n, tile_rows) + std::min(n, N)};
+    if (use_tiles) LAUNCH(RG_K_SETUP, launch_row_tiles(pol->row_tab, pol->coff, (int)r0, n, tile_rows, pol->tile_r0,
                                                        pol->tile_nr, d_tiles, st));
     if ((rc = run_layers(pol, st, d_chunk, n, ctx_all, true, nullptr, use_tiles ? &rt : nullptr))) return rc;
     for (int h0 = 0; h0 < n; h0 += slice) {

@@ -638,8 +638,14 @@ __global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_prefix(con
 // row i sees tokens 0 .. row_pos of its row (causal mask per column).  The
 // whole context is one work item, so the normalised output goes straight to
 // the activation planes.
+constexpr int ATT_TILE_MAX_WAVES = 12;
+
+// Positions per row tile: 32 while the tile's query rows (positions x GQA
+// heads) fit ATT_TILE_MAX_WAVES waves of 16, else 16.
+int att_tile_rows_for(int rep) { return 32 * rep <= 16 * ATT_TILE_MAX_WAVES ? 32 : 16; }
+
 template <int HD>
-__global__ __launch_bounds__(64 * ATT_PRE_MAX_WAVES) void k_attention_tile(
+__global__ __launch_bounds__(64 * ATT_TILE_MAX_WAVES) void k_attention_tile(
     const float* __restrict__ q, int n_q, int n_kv, const bf16_t* __restrict__ pool, KvGeom g, int layer,
     const int32_t* __restrict__ page_tab, int tab_stride, const int32_t* __restrict__ row_tab,
     const int32_t* __restrict__ row_pos, const int32_t* __restrict__ tile_r0, const int32_t* __restrict__ tile_nr,
@@ -877,8 +883,9 @@ hipError_t launch_attention_tile(const float* q, int n_q, int n_kv, int head_dim
                                  hipStream_t st) {
   if (tiles_ub <= 0) return hipSuccess;
   const int rep = n_q / n_kv;
-  if (rep * 16 > 16 * ATT_PRE_MAX_WAVES || max_ctx > 16 * ATT_MAX_CHUNK_PAGES) return hipErrorInvalidValue;
-  const int waves = std::max(4, rep);
+  const int rows = att_tile_rows_for(rep);
+  if (rows * rep > 16 * ATT_TILE_MAX_WAVES || max_ctx > 16 * ATT_MAX_CHUNK_PAGES) return hipErrorInvalidValue;
+  const int waves = std::max(4, (rows * rep + 15) / 16);
   const int64_t items = (int64_t)tiles_ub * n_kv;
   const unsigned blocks = (unsigned)((items + 7) / 8 * 8);
   const ActOut o{out, a_plane};
@@ -892,3 +899,5 @@ hipError_t launch_attention_tile(const float* q, int n_q, int n_kv, int head_dim
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
+
+int att_tile_rows(int n_q, int n_kv) { return att_tile_rows_for(n_q / n_kv); }

@@ -97,11 +97,11 @@ __global__ __launch_bounds__(256) void k_recompute_rows(RecomputeRows a, const T
 }
 
 // Tiles of the chunk's rows for the row-tile attention: each sequence's rows
-// in the chunk, cut into runs of 16 from its first row.  One block of 1024
+// in the chunk, cut into runs of tr from its first row.  One block of 1024
 // threads; tile k starts at row tile_r0[k] and has tile_nr[k] rows, in row
 // order; *d_tiles gets the count.
 __global__ __launch_bounds__(1024) void k_row_tiles(const int32_t* __restrict__ row_tab,
-                                                    const int32_t* __restrict__ coff, int row0, int n,
+                                                    const int32_t* __restrict__ coff, int row0, int n, int tr,
                                                     int32_t* __restrict__ tile_r0, int32_t* __restrict__ tile_nr,
                                                     int* __restrict__ d_tiles) {
   __shared__ int lds[17];
@@ -113,8 +113,8 @@ __global__ __launch_bounds__(1024) void k_row_tiles(const int32_t* __restrict__ 
       const int s = row_tab[r];
       const int f = max(coff[s] - row0, 0);         // the sequence's first row in this chunk
       const int e = min(coff[s + 1] - row0, n);     // one past its last
-      flag = ((r - f) & 15) == 0;
-      len = min(16, e - r);
+      flag = (r - f) % tr == 0;
+      len = min(tr, e - r);
     }
     int tot;
     const int o = block_excl_scan(flag, lds, &tot) + carry;
@@ -286,9 +286,10 @@ hipError_t launch_recompute_rows(int dtype, const void* embed, const RecomputeRo
   return hipGetLastError();
 }
 
-hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row0, int n, int32_t* tile_r0,
-                            int32_t* tile_nr, int* d_tiles, hipStream_t st) {
-  hipLaunchKernelGGL(k_row_tiles, dim3(1), dim3(1024), 0, st, row_tab, coff, row0, n, tile_r0, tile_nr, d_tiles);
+hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row0, int n, int tile_rows,
+                            int32_t* tile_r0, int32_t* tile_nr, int* d_tiles, hipStream_t st) {
+  hipLaunchKernelGGL(k_row_tiles, dim3(1), dim3(1024), 0, st, row_tab, coff, row0, n, tile_rows, tile_r0, tile_nr,
+                     d_tiles);
   return hipGetLastError();
 }
 

@@ -135,7 +135,7 @@ hipError_t launch_attention_prefix(const float* q, int n_q, int n_kv, int head_d
                                    int max_group_rows, AttPlan plan, float* part_o, float* part_ml, hipStream_t st);
 
 // Row-tile pass (bf16 models, prefill-style rows): tile k = rows tile_r0[k] ..
-// + tile_nr[k] - 1 (at most 16) of one page table row at consecutive
+// + tile_nr[k] - 1 (at most att_tile_rows) of one page table row at consecutive
 // positions; every query row attends causally to positions 0..row_pos of its
 // row and the normalised output goes to the activation planes `out`.
 // *d_tiles <= tiles_ub tiles; max_ctx bounds every row's context.
@@ -260,8 +260,10 @@ hipError_t launch_recompute_rows(int dtype, const void* embed, const RecomputeRo
 // Cuts rows 0..n-1 of a recompute chunk (row_tab = sequence, coff = row
 // offsets, row0 = the chunk's first global row) into per-sequence tiles of at
 // most 16 rows for the row-tile attention.
-hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row0, int n, int32_t* tile_r0,
-                            int32_t* tile_nr, int* d_tiles, hipStream_t st);
+hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row0, int n, int tile_rows,
+                            int32_t* tile_r0, int32_t* tile_nr, int* d_tiles, hipStream_t st);
+// Positions per row tile the row-tile attention takes for this GQA shape.
+int att_tile_rows(int n_q, int n_kv);
 hipError_t launch_first_rows(const int32_t* tokens, const int32_t* seq_grp, int n_seq, int max_new, int V,
                              int32_t* lrow, int32_t* tgt, int32_t* out, int32_t* bad_token, hipStream_t st);
 // lp[out[r]] = z[tgt[r]]/T - logsumexp(z/T), z = logits row lrow[r] (lrow NULL: r).
