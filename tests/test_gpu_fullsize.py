@@ -1,16 +1,18 @@
 """Parity at the benchmark's full size: the 1.5B workload exactly as bench.py
 times it (32 prompts x G = 16, 512-token prompts, max_new 4096, forced
-lognormal lengths, seed 1234), checked on outputs the oracle can compute one
-by one and on properties that hold at any size.
+lognormal lengths, seed 1234), and the same shape with a seeded group size
+per prompt drawn from {4, 8, 16, 32} (a ragged batch of groups), checked on
+outputs the oracle can compute one by one and on properties that hold at any
+size.
 
-* every one of the 512 retired lengths equals its forced length, and every
+* every retired length equals its forced length, and every
   completion has the required structure (EOS last, padding, finite logprobs);
-* prompt 0's 16 siblings over their first three steps: the library's raw
+* prompt 0's siblings (16, or its drawn G) over their first three steps: the library's raw
   logits within 1e-2 (max-abs) of the fp64 oracle's, and its tokens equal to
   the oracle's free-running ones except where the oracle's top-2 margin is
   below 1e-2;
 * the teacher-forced recompute reproduces the rollout's log-probabilities
-  over all 770,996 completion tokens (within 2e-2).
+  over every completion token (770,996 of them at G = 16; within 2e-2).
 """
 import numpy as np
 import pytest
@@ -25,11 +27,12 @@ STEPS = 3
 
 
 @pytest.mark.timeout(400)
-def test_full_1p5b_workload_sampled_against_oracle():
+@pytest.mark.parametrize("name", ["1.5b", "1.5b-dyn"])
+def test_full_1p5b_workload_sampled_against_oracle(name):
     import torch
     assert torch.cuda.is_available()
     import paper_2606_02218_amd as rg
-    wl = get_config("1.5b")
+    wl = get_config(name)
     shape = wl.shape
     w = make_weights(shape, 0)
     inp = make_inputs(wl, 0)
@@ -71,4 +74,4 @@ def test_full_1p5b_workload_sampled_against_oracle():
             assert abs(lp_np[s, t] - ref["logprobs"][s, t]) <= 2 * LOGIT_TOL
     print(f"worst logit gap {worst:.2e} over prompt 0's siblings, {split} split at a low margin", flush=True)
     assert worst <= LOGIT_TOL, worst
-    assert split <= 2, split
+    assert split <= max(2, g0 // 8), split
