@@ -305,8 +305,10 @@ def main():
     weights = make_weights(shape, 0)
     inp = make_inputs(wl, 0)
     N = inp.n_seq
+    print(f"# weights and inputs of {wl.name} ready ({N} sequences)", file=sys.stderr, flush=True)
     pol = rg.Policy(shape, weights, max_seqs=N, max_prompts=wl.n_prompts,
                     max_prompt_tokens=wl.n_prompts * wl.prompt_len, max_context=wl.prompt_len + wl.max_new)
+    print(f"# policy ready: {pol.device_bytes() / 2**30:.1f} GiB on the device", file=sys.stderr, flush=True)
     dev = torch.device("cuda")
     prompts = torch.from_numpy(inp.prompts).to(dev)
     G_dev = torch.from_numpy(inp.G).to(dev)
@@ -356,7 +358,8 @@ def main():
            "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_per_step, 2), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "bf16", "data": "synthetic",
-           "config": {"workload": wl.name, "prompts": wl.n_prompts, "group_size": int(inp.G[0]),
+           "config": {"workload": wl.name, "prompts": wl.n_prompts,
+                      "group_size": wl.group_size if wl.group_size is not None else sorted(set(int(g) for g in inp.G)),
                       "sequences": N, "prompt_len": wl.prompt_len, "max_new": wl.max_new,
                       "generated_tokens": gen, "decode_steps": int(len(hist_a)),
                       "group_prefix_pass": bool(args.group_prefix)},
