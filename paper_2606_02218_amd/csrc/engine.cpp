@@ -119,6 +119,7 @@ struct rg_policy {
 
   hipStream_t cap_st = nullptr;   // private stream used only to capture decode-step graphs
   bool use_graphs = true;
+  int progress_every = 0;   // RG_PROGRESS=N: a stderr line every N enqueued decode steps
 
   int alloc(void** p, size_t bytes) {
     bytes = std::max<size_t>(bytes, 256);
@@ -774,6 +775,8 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
     if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipStreamCreate: ") + hipGetErrorString(e)));
     const char* env = getenv("RG_NO_GRAPHS");
     pol->use_graphs = !(env && env[0] == '1');
+    const char* pe = getenv("RG_PROGRESS");
+    pol->progress_every = pe ? std::max(0, atoi(pe)) : 0;
   }
   *out = pol;
   return RG_OK;
@@ -890,6 +893,10 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
     }
     if ((rc = snapshot(t))) return rc;
     last_t = t;
+    if (pol->progress_every && t % pol->progress_every == 0) {
+      fprintf(stderr, "# decode step %d enqueued; step %d done with %d active rows\n", t, known_t, m_ub);
+      fflush(stderr);
+    }
   }
   HIPTRY(hipStreamSynchronize(st));
   // snapshots the loop has not read yet (at most RG_LOOKAHEAD of them)

@@ -1,0 +1,46 @@
+"""Host logic of bench.py that needs no GPU: the measured HBM traffic of the
+roofline kernel is reported from its committed counter summary only for the
+workload and kernel class it was measured on, and only while the sources it
+was measured on are unchanged."""
+import importlib.util
+import os
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_traffic_summary_value(bench, monkeypatch):
+    # the machine-read value is the summary's scaled counters: FETCH (226,569 KiB)
+    # + WRITE (2,388 KiB) per launch; with the current sources it is either that
+    # value or, once they have changed, None
+    want = (226569 + 2388) * 1024
+    assert bench.measured_traffic("1.5b", "attn") in (want, None)
+    import re
+    text = open(os.path.join(ROOT, bench.TRAFFIC_SUMMARY)).read()
+    digest = re.search(r"^\s*sources_sha256:\s*(\S+)", text, re.M).group(1)
+    monkeypatch.setattr(bench, "sources_sha256", lambda paths=None: digest)
+    assert bench.measured_traffic("1.5b", "attn") == want
+
+
+def test_traffic_only_for_its_workload_and_kernel(bench):
+    assert bench.measured_traffic("7b", "attn") is None
+    assert bench.measured_traffic("1.5b", "gemm_gu") is None
+
+
+def test_traffic_dropped_when_sources_change(bench, monkeypatch):
+    monkeypatch.setattr(bench, "sources_sha256", lambda paths=None: "0" * 64)
+    assert bench.measured_traffic("1.5b", "attn") is None
+
+
+def test_traffic_absent_summary(bench, monkeypatch):
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", "profiles/no_such_summary.md")
+    assert bench.measured_traffic("1.5b", "attn") is None
