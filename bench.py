@@ -55,7 +55,7 @@ def algorithmic_bytes(shape, hist_active, hist_groups, hist_ctx, plen):
 
 
 def decode_bytes_total(shape, hist_active, hist_groups, hist_ctx):
-    """SURVEY-style whole-step decode bytes: weights + KV read + per-row write."""
+    """Whole-step decode bytes: weights + KV read + per-row write."""
     W = shape.decode_weight_bytes()
     kv_tok = shape.kv_bytes_per_token()
     tot = 0.0
