@@ -204,6 +204,18 @@ def test_errors(torch):
     with pytest.raises(rg.RolloutError) as e:
         pol.rollout(bad, [2], 4, 0)
     assert e.value.code == RG_EINVAL
+    three = prompts_to_device([np.arange(4, dtype=np.int32)] * 3)
+    with pytest.raises(rg.RolloutError) as e:        # 3 prompts > max_prompts = 2
+        pol.rollout(three, [1, 1, 1], 4, 0)
+    assert e.value.code == RG_ENOMEM and "max_prompts" in str(e.value)
+    long2 = prompts_to_device([np.arange(20, dtype=np.int32), np.arange(20, dtype=np.int32)])
+    with pytest.raises(rg.RolloutError) as e:        # 40 prompt tokens > max_prompt_tokens = 32
+        pol.rollout(long2, [1, 1], 4, 0)
+    assert e.value.code == RG_ENOMEM and "prompt tokens" in str(e.value)
+    for T in (0.0, -1.0, float("nan"), float("inf")):
+        with pytest.raises(rg.RolloutError) as e:
+            pol.rollout(p, [4], 8, 0, temperature=T)
+        assert e.value.code == RG_EINVAL and "temperature" in str(e.value), T
     # the policy is still usable after errors
     tok, ln, lp = pol.rollout(p, [4], 8, 0, forced_len=[8, 8, 8, 8])
     np.testing.assert_array_equal(_np(ln), [8, 8, 8, 8])
