@@ -327,8 +327,8 @@ def main():
         loss_forward(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (groups would shard across GPUs "
-              "by prompt; see the design notes).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (prompt groups would shard "
+              "across GPUs, one process per GPU; see the design notes).", file=sys.stderr)
         sys.exit(2)
 
     import torch

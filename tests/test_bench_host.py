@@ -44,3 +44,13 @@ def test_traffic_dropped_when_sources_change(bench, monkeypatch):
 def test_traffic_absent_summary(bench, monkeypatch):
     monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", "profiles/no_such_summary.md")
     assert bench.measured_traffic("1.5b", "attn") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    # the refusal comes before torch touches a device, so it runs anywhere
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
