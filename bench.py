@@ -260,9 +260,10 @@ def loss_forward(args):
 # HBM traffic of the roofline kernel comes from rocprofv3 counter passes that
 # cannot run inside this process (they slow every dispatch); their result is
 # kept as a text summary and reported only while the sources it was measured
-# on are unchanged.
+# on are unchanged: the attention kernels with their launch mapping and chunk
+# plan, and the shared device and kernel headers.
 TRAFFIC_SOURCES = ["paper_2606_02218_amd/csrc/k_attn.hip", "paper_2606_02218_amd/csrc/rg_device.h",
-                   "paper_2606_02218_amd/csrc/rg_kernels.h", "paper_2606_02218_amd/csrc/engine.cpp"]
+                   "paper_2606_02218_amd/csrc/rg_kernels.h"]
 TRAFFIC_SUMMARY = "profiles/attention_decode_1.5b_traffic.md"
 
 

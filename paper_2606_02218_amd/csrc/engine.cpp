@@ -43,7 +43,6 @@ constexpr int RG_PAGE_TOK = 16;        // tokens per KV page
 constexpr int RG_SPLIT_MAX = GEMM_MAX_SPLITS;   // largest split-K factor of a decode GEMM
 constexpr int RG_GEMM_TARGET = 384;    // blocks a split-K GEMM launch aims for
 constexpr int RG_GEMM_FULL = 256;      // output-tile blocks that need no split
-constexpr int RG_ATT_TARGET = 1024;    // work items (waves) an attention launch aims for
 constexpr int RG_PRE_TARGET = 512;     // workgroups the prefix attention pass aims for
 constexpr int RG_PRE_MIN_CHUNK = 64;   // fewest prefix tokens per prefix workgroup
 constexpr int RG_PRE_MAX_SLOTS = 16;   // prefix chunks per row (more only for prefixes > 16k tokens)
@@ -295,13 +294,7 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
                const PrefixPass* pre, const RowTiles* tiles = nullptr) {
   if (rows_ub <= 0) return RG_OK;
   const int tab_stride = pol->max_pages;
-  // chunks per row: about RG_ATT_TARGET work items (fewer, longer chunks
-  // measured faster than filling every wave slot: less partial traffic and
-  // per-item set-up), at least ~256 tokens each for the longest context, at
-  // most 16384 tokens each
-  const int64_t items = (int64_t)rows_ub * pol->nkv;
-  int n_chunks = (int)std::min<int64_t>((RG_ATT_TARGET + items / 2) / items, ceil_div(ctx_max, 256));
-  n_chunks = std::max<int>({1, n_chunks, (int)ceil_div(ctx_max, 16000)});
+  const int n_chunks = att_row_chunks(rows_ub, pol->nkv, ctx_max);
   AttPlan plan{n_chunks, 0, 0, n_chunks};
   if (pre && pre->max_pref > 0) {
     // prefix chunks: about RG_PRE_TARGET workgroups, at least RG_PRE_MIN_CHUNK
@@ -421,7 +414,10 @@ int enqueue_step(rg_policy* pol, hipStream_t st, int rows_ub, int ctx_max, Sampl
 // A decode-step graph per row bucket, captured on first use in a rollout.
 struct StepGraphs {
   std::vector<std::pair<int, hipGraphExec_t>> execs;
+  hipStream_t launched_on = nullptr;   // set once a graph has been launched
   ~StepGraphs() {
+    // an early error return may leave replays in flight: let them finish first
+    if (launched_on) (void)hipStreamSynchronize(launched_on);
     for (auto& g : execs) (void)hipGraphExecDestroy(g.second);
   }
 };
@@ -707,7 +703,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   const int64_t M = pol->m_act, S = lim.max_seqs, P = lim.max_prompts;
   const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
   pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
-  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + RG_ATT_TARGET +
+  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + ATT_ITEMS_TARGET +
                        S * (RG_PRE_MAX_SLOTS + ceil_div(lim.max_context, 1024));
   pol->hist_cap = lim.max_context;
   struct Piece { void** p; size_t bytes; };
@@ -887,6 +883,7 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
     if (graphs_on) {
       hipGraphExec_t exec;
       if ((rc = step_graph(pol, graphs, rows_ub, ctx_all, sm, ca, pre, &exec))) return rc;
+      graphs.launched_on = st;
       HIPTRY(hipGraphLaunch(exec, st));
     } else {
       if ((rc = enqueue_step(pol, st, rows_ub, ctx_all, sm, ca, pre))) return rc;

@@ -901,3 +901,12 @@ hipError_t launch_attention_tile(const float* q, int n_q, int n_kv, int head_dim
 }
 
 int att_tile_rows(int n_q, int n_kv) { return att_tile_rows_for(n_q / n_kv); }
+
+// About ATT_ITEMS_TARGET work items (fewer, longer chunks measured faster than
+// filling every wave slot: less partial traffic and per-item set-up), at least
+// ~256 tokens each for the longest context, at most 16000 tokens each.
+int att_row_chunks(int rows_ub, int n_kv, int ctx_max) {
+  const int64_t items = (int64_t)rows_ub * n_kv;
+  int n = (int)std::min<int64_t>((ATT_ITEMS_TARGET + items / 2) / items, (ctx_max + 255) / 256);
+  return std::max<int>({1, n, (ctx_max + 15999) / 16000});
+}

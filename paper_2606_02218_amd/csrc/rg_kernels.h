@@ -264,6 +264,11 @@ hipError_t launch_row_tiles(const int32_t* row_tab, const int32_t* coff, int row
                             int32_t* tile_r0, int32_t* tile_nr, int* d_tiles, hipStream_t st);
 // Positions per row tile the row-tile attention takes for this GQA shape.
 int att_tile_rows(int n_q, int n_kv);
+// Work items (waves) a per-row attention launch aims for.
+constexpr int ATT_ITEMS_TARGET = 1024;
+// Context chunks per row for a per-row attention launch over rows_ub rows
+// whose contexts are at most ctx_max tokens.
+int att_row_chunks(int rows_ub, int n_kv, int ctx_max);
 hipError_t launch_first_rows(const int32_t* tokens, const int32_t* seq_grp, int n_seq, int max_new, int V,
                              int32_t* lrow, int32_t* tgt, int32_t* out, int32_t* bad_token, hipStream_t st);
 // lp[out[r]] = z[tgt[r]]/T - logsumexp(z/T), z = logits row lrow[r] (lrow NULL: r).

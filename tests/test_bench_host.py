@@ -19,13 +19,21 @@ def bench():
 
 
 def test_traffic_summary_value(bench, monkeypatch):
-    # the machine-read value is the summary's scaled counters: FETCH (226,569 KiB)
-    # + WRITE (2,388 KiB) per launch; with the current sources it is either that
-    # value or, once they have changed, None
-    want = (226569 + 2388) * 1024
-    assert bench.measured_traffic("1.5b", "attn") in (want, None)
+    # the machine-read value is the table's scaled FETCH_SIZE + WRITE_SIZE per
+    # dispatch (KiB); with the current sources it is that value or, once they
+    # have changed, None
     import re
     text = open(os.path.join(ROOT, bench.TRAFFIC_SUMMARY)).read()
+    scaled = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        cal, scale, raw, out = re.search(r"^\| %s \| ([\d,.]+) KiB \| ([\d.]+) \| ([\d,.]+) KiB \| ([\d,]+) KiB \|" % c,
+                                         text, re.M).groups()
+        f = lambda s: float(s.replace(",", ""))
+        assert abs(f(raw) * f(scale) - f(out)) <= 1.0, c
+        scaled[c] = f(raw) * f(scale)
+    want = int(re.search(r"^\s*traffic_bytes_per_launch:\s*(\d+)", text, re.M).group(1))
+    assert abs(want - (scaled["FETCH_SIZE"] + scaled["WRITE_SIZE"]) * 1024) <= 1024
+    assert bench.measured_traffic("1.5b", "attn") in (want, None)
     digest = re.search(r"^\s*sources_sha256:\s*(\S+)", text, re.M).group(1)
     monkeypatch.setattr(bench, "sources_sha256", lambda paths=None: digest)
     assert bench.measured_traffic("1.5b", "attn") == want
