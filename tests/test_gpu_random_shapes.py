@@ -8,6 +8,8 @@ forced lengths up to max_new), then checks:
 * the rollout teacher-forced on the oracle's tokens: every logit within 1e-2
   (bf16) / 1e-4 (fp32) of the oracle's, log-probabilities within twice that,
   sampling decisions equal except at top-2 margins below 1e-2, lengths exact;
+* free-running from the same inputs follows the oracle's trajectory (tokens
+  equal up to the first position whose oracle margin is below 1e-2);
 * the recompute of the oracle's tokens against the oracle's teacher-forced
   log-probabilities (same tolerance), zero past each length.
 
@@ -23,7 +25,7 @@ import pytest
 from oracle.grpo import teacher_forced_logprobs
 from oracle.rollout import rollout as oracle_rollout
 from workload import ModelShape, make_weights
-from rg_helpers import oracle_for, make_policy, prompts_to_device, MARGIN_TOL
+from rg_helpers import oracle_for, make_policy, prompts_to_device, compare_free_running, check_structure, MARGIN_TOL
 
 pytestmark = pytest.mark.gpu
 
@@ -81,6 +83,10 @@ def test_random_shape_against_oracle(i):
             assert abs(float(lp[s, t]) - float(ref["logprobs"][s, t])) <= 2 * tol, (s, t)
             if tok[s, t] != ref["tokens"][s, t]:
                 assert ref["margins"][s, t] < MARGIN_TOL, (s, t, ref["margins"][s, t])
+    tok2, ln2, lp2 = pol.rollout(dp, G, max_new, 77 + i, forced_len=L)
+    tok2, ln2, lp2 = tok2.cpu().numpy(), ln2.cpu().numpy(), lp2.cpu().numpy()
+    check_structure(tok2, ln2, lp2, shape.eos_id, max_new, L)
+    compare_free_running(tok2, lp2, ref, ln2, lp_tol=2 * tol)
     want = teacher_forced_logprobs(model, prompts, G, ref["tokens"], ref["lengths"])
     got = pol.recompute_logprobs(dp, G, ft, torch.from_numpy(ref["lengths"]).cuda()).cpu().numpy()
     valid = np.arange(max_new)[None, :] < ref["lengths"][:, None]
