@@ -50,6 +50,7 @@ constexpr int RG_RING = 64;            // async active-count slots
 constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last seen count
 constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
 constexpr int RG_SAMPLE_SLICES_MAX = 32;  // vocabulary slices per sampled row
+constexpr int RG_LM_SLICE_ROWS = 2048;    // recompute: lm-head rows per slice (when the activations hold them)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -85,6 +86,7 @@ struct rg_policy {
   float* att_o = nullptr;
   float* att_ml = nullptr;
   int64_t att_rowchunks = 0;
+  int64_t logit_rows = 0;   // rows of the fp32 logits buffer
   float* logits = nullptr;
   float* sample_part = nullptr;   // [rows][RG_SAMPLE_SLICES_MAX][4]
   int32_t *page_tab = nullptr, *seq_grp = nullptr, *seq_npages = nullptr, *seq_nshared = nullptr,
@@ -701,6 +703,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
 
   // ---- workspace
   const int64_t M = pol->m_act, S = lim.max_seqs, P = lim.max_prompts;
+  // the rollout needs max(S, P) rows of logits; the recompute's lm head runs
+  // in slices of this many rows, and slices above 1024 rows take the 256 x 256
+  // projection tiles
+  pol->logit_rows = std::max<int64_t>({S, P, std::min<int64_t>(M, RG_LM_SLICE_ROWS)});
   const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
   pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
   pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + ATT_ITEMS_TARGET +
@@ -717,7 +723,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       {(void**)&pol->qbuf, (size_t)(M * pol->q_dim * 4)},
       {(void**)&pol->att_o, (size_t)(pol->att_rowchunks * pol->nq * pol->hd * 4)},
       {(void**)&pol->att_ml, (size_t)(pol->att_rowchunks * pol->nq * 2 * 4)},
-      {(void**)&pol->logits, (size_t)(std::max(S, P) * pol->V * 4)},
+      {(void**)&pol->logits, (size_t)(pol->logit_rows * pol->V * 4)},
       {(void**)&pol->sample_part, (size_t)(std::max(S, P) * RG_SAMPLE_SLICES_MAX * 4 * 4)},
       {(void**)&pol->page_tab, (size_t)((S + P) * pol->max_pages * 4)},
       {(void**)&pol->seq_grp, (size_t)(S * 4)},
@@ -951,7 +957,7 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
   // the teacher-forced rows in chunks of m_act; the lm head in slices of the
   // logits buffer's rows
   const int chunk = pol->m_act;
-  const int slice = (int)std::max<int64_t>(pol->lim.max_seqs, pol->lim.max_prompts);
+  const int slice = (int)pol->logit_rows;
   const int ctx_all = gr.max_plen + max_new;
   const size_t row_bytes = (size_t)pol->d * pol->eb;
   int* d_chunk = pol->state + 11;
