@@ -24,6 +24,7 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
   const int L = a.forced_len ? a.forced_len[s] : -1;
   const bool mask_eos = L > 0 && t < L - 1;
   const float T = a.temperature;
+  const bool unit_T = T == 1.0f;                            // z / 1 == z exactly: skip the division
   const int nb = a.V >> 3;                                  // 8-token Philox blocks
   const int per = (nb + a.n_slices - 1) / a.n_slices;
   const int vb0 = blockIdx.x * per, vb1 = min(nb, vb0 + per);
@@ -41,12 +42,17 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int v = vb * 8 + j;
-      const float zt = zz[j] / T;
-      if (zt > m) { sum = sum * expf(m - zt) + 1.f; m = zt; }
-      else sum += expf(zt - m);
+      const float zt = unit_T ? zz[j] : zz[j] / T;
+      // running logsumexp: the hardware exponential (relative error ~1e-7)
+      if (zt > m) { sum = sum * __expf(m - zt) + 1.f; m = zt; }
+      else sum += __expf(zt - m);
       const uint32_t bits = (uint32_t)(w.v[j >> 1] >> (32 * (j & 1)));
       const float u = rg_uniform_from_bits(bits);
-      float sc = zt + (-logf(-logf(u)));
+      // Gumbel noise -log(-log u): the inner log keeps full accuracy (for u
+      // near 1 its result is ~6e-8, where only a relative-error log is safe);
+      // the outer one takes an argument in [6e-8, 16.7] and needs ~1e-7
+      // absolute accuracy, which the hardware logarithm gives
+      float sc = zt + (-__logf(-logf(u)));
       if (mask_eos && v == a.eos) sc = -INFINITY;
       if (sc > best || (sc == best && v < best_v)) { best = sc; best_v = v; }
     }
