@@ -11,6 +11,7 @@
 * the group prefix pass (each prompt's full prefix pages attended once per
   group) agrees with the row-by-row pass within rounding and with the oracle,
   also for a group larger than one prefix workgroup's 128 query rows.
+* temperatures other than 1 (0.7, 1.6): free-running and teacher-forced.
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -49,14 +50,15 @@ def _case(shape, seed, plens, G, max_new, len_range):
     return prompts, L
 
 
-def _run_tf(torch, shape, w, prompts, G, max_new, L, seed, share=True, group_prefix=False):
+def _run_tf(torch, shape, w, prompts, G, max_new, L, seed, share=True, group_prefix=False, temperature=1.0):
     model = oracle_for(shape, w)
-    ref = oracle_rollout(model, prompts, G, max_new, seed, L, record_steps=max_new)
+    ref = oracle_rollout(model, prompts, G, max_new, seed, L, record_steps=max_new, temperature=temperature)
     pol = make_policy(shape, w, max_seqs=int(np.sum(G)), max_prompts=len(G), max_prompt_tokens=int(sum(map(len, prompts))),
                       max_context=max(map(len, prompts)) + max_new)
     ft = torch.from_numpy(ref["tokens"]).cuda()
     tok, ln, lp, dump = pol.rollout(prompts_to_device(prompts), G, max_new, seed, forced_len=L, force_tokens=ft,
-                                    dump_steps=max_new, share_prefix=share, group_prefix_pass=group_prefix)
+                                    dump_steps=max_new, share_prefix=share, group_prefix_pass=group_prefix,
+                                    temperature=temperature)
     torch.cuda.synchronize()
     return ref, _np(tok), _np(ln), _np(lp), _np(dump), pol
 
@@ -91,6 +93,27 @@ def test_tiny_free_running(torch, seed):
     check_structure(tok, ln, lp, wl.shape.eos_id, wl.max_new, inp.forced_len)
     checked, split = compare_free_running(tok, lp, ref, ln, lp_tol=1e-4)
     assert checked > 0
+
+
+@pytest.mark.parametrize("T", [0.7, 1.6])
+def test_temperature_other_than_one(torch, T):
+    # at T != 1 the sampler scales the logits by 1/T (at T = 1 it takes them as
+    # they are): sampling decisions and log-probabilities against the oracle
+    wl = get_config("tiny")
+    w = make_weights(wl.shape, 1)
+    inp = make_inputs(wl, 1)
+    ref = oracle_rollout(oracle_for(wl.shape, w), inp.prompts, inp.G, wl.max_new, 3, inp.forced_len, temperature=T)
+    pol = make_policy(wl.shape, w, 16, 4, 64, wl.prompt_len + wl.max_new)
+    tok, ln, lp = pol.rollout(prompts_to_device(inp.prompts), inp.G, wl.max_new, 3, forced_len=inp.forced_len,
+                              temperature=T)
+    tok, ln, lp = _np(tok), _np(ln), _np(lp)
+    check_structure(tok, ln, lp, wl.shape.eos_id, wl.max_new, inp.forced_len)
+    checked, _ = compare_free_running(tok, lp, ref, ln, lp_tol=1e-4)
+    assert checked > 0
+    wb = make_weights(GQA, 4)
+    prompts, L = _case(GQA, 4, [33, 12], [5, 3], 16, (1, 16))
+    ref, tok, ln, lp, dump, _ = _run_tf(torch, GQA, wb, prompts, [5, 3], 16, L, 13, temperature=T)
+    _check_tf(ref, tok, ln, lp, dump, L)
 
 
 def test_tiny_teacher_forced(torch):
