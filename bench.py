@@ -201,14 +201,16 @@ def loss_forward(args):
     G_dev = torch.from_numpy(inp.G).to(dev)
     rewards = torch.from_numpy(inp.rewards).to(dev)
     tokens, lengths, lp_roll = pol.rollout(prompts, inp.G, wl.max_new, 1234, forced_len=inp.forced_len)
-    adv = rg.group_advantage(rewards, G_dev, 1e-6, 1)
-    keep, _, _ = rg.group_filter(rewards, G_dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
     ln_np = lengths.cpu().numpy()
     old = torch.from_numpy(drifted_logprobs(lp_roll.cpu().numpy(), ln_np, 0, 0.1)).to(dev)
     new = torch.empty_like(lp_roll)
     print("# rollout done", file=sys.stderr, flush=True)
 
     def step(prof):
+        # advantage and zero-variance filter of the group rewards, then the loss forward
+        rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)
+        keep, _, _ = rg.group_filter(rewards, G_dev)
         pol.recompute_logprobs(prompts, inp.G, tokens, lengths, profile=prof, out=new)
         return rg.grpo_surrogate(new, old, adv, lengths, G_dev, 0.2, 0.28, "token", keep)
 
@@ -230,7 +232,26 @@ def loss_forward(args):
     loss = out.cpu().numpy()
     scored = int(ln_np.sum())
     ms = dt / args.steps * 1e3
-    res = {"metric": "GRPO loss-forward scored tokens/s (recompute_logprobs + grpo_surrogate)",
+    keep, _, _ = rg.group_filter(rewards, G_dev)
+
+    def per_call_us(fn, reps=200):
+        # back-to-back calls on torch's current stream, which the library launches on
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+
+    small = {"group_advantage": per_call_us(lambda: rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)),
+             "group_filter": per_call_us(lambda: rg.group_filter(rewards, G_dev)),
+             "grpo_surrogate": per_call_us(lambda: rg.grpo_surrogate(new, old, adv, lengths, G_dev, 0.2, 0.28,
+                                                                     "token", keep))}
+    res = {"metric": "GRPO loss-forward scored tokens/s (group_advantage + group_filter + recompute_logprobs + "
+                     "grpo_surrogate)",
            "value": round(scored / (ms / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(ms, 2), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
@@ -238,7 +259,8 @@ def loss_forward(args):
                       "scored_tokens": scored},
            "surrogate": {"loss": float(loss[0]), "clip_frac": float(loss[1]), "tokens": int(loss[2]),
                          "sequences": int(loss[3])},
-           "recompute_vs_rollout_logprob_max_abs": round(dev_max, 5)}
+           "recompute_vs_rollout_logprob_max_abs": round(dev_max, 5),
+           "small_calls_us": small}
     if breakdown:
         res["kernel_ms_breakdown"] = {f"{'prefill' if ph == 0 else 'rows'}.{k}": round(v[0], 1)
                                       for ph in (0, 1) for k, v in sorted(breakdown[ph].items(), key=lambda kv: -kv[1][0])
