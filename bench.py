@@ -286,7 +286,7 @@ def loss_forward(args):
 # plan, and the shared device and kernel headers.
 TRAFFIC_SOURCES = ["paper_2606_02218_amd/csrc/k_attn.hip", "paper_2606_02218_amd/csrc/rg_device.h",
                    "paper_2606_02218_amd/csrc/rg_kernels.h"]
-TRAFFIC_SUMMARY = "profiles/attention_decode_1.5b_traffic.md"
+TRAFFIC_SUMMARY = "profiles/attention_decode_1.5b_traffic.txt"
 
 
 def sources_sha256(paths=TRAFFIC_SOURCES):

@@ -62,3 +62,22 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_traffic_summary_ships_with_the_tree(bench):
+    # the bench reads this summary at run time, so no pattern that keeps files
+    # off the GPU machines may match it (tar-style: a pattern without a slash
+    # matches the file name at any depth; './x' only from the top)
+    import fnmatch
+    ignore = os.path.join(ROOT, ".gpurunignore")
+    if not os.path.exists(ignore):
+        return
+    rel = bench.TRAFFIC_SUMMARY
+    for pat in (l.strip() for l in open(ignore)):
+        if not pat or pat.startswith("#"):
+            continue
+        if pat.startswith("./"):
+            p = pat[2:].rstrip("/")
+            assert not (rel == p or rel.startswith(p + "/") or fnmatch.fnmatch(rel, p)), pat
+        else:
+            assert not fnmatch.fnmatch(os.path.basename(rel), pat) and not fnmatch.fnmatch(rel, pat), pat
