@@ -156,7 +156,10 @@ const char* rg_last_error(void);
  * the weights, allocates the workspace and KV pool for `limits` on the current
  * device.  *out receives the handle.  Errors: RG_EINVAL (NULL arguments,
  * non-positive sizes), RG_EUNSUPPORTED (shape), RG_ENOMEM / RG_EHIP
- * (allocation). */
+ * (allocation).  Read once here from the environment: RG_NO_GRAPHS=1 makes
+ * rollout_group launch its decode steps directly instead of replaying
+ * captured HIP graphs (the same kernels and arguments); RG_PROGRESS=N prints
+ * a line to stderr every N decode steps of rollout_group. */
 int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits* limits,
                      rg_policy** out);
 void rg_policy_destroy(rg_policy* pol);   /* NULL is a no-op */
