@@ -122,3 +122,16 @@ def test_argument_validation_cases_without_gpu():
     assert lib.rg_philox_blocks(1, 2, p[0], -1, p[1], None) == E
     assert lib.rg_gumbel_bits(1, 0, 0, 0, p[0], None) == E
     assert lib.rg_gumbel_bits(1, -1, 0, 16, p[0], None) == E
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    """Without librollout.so every entry point raises: there is no fallback."""
+    from paper_2606_02218_amd import _lib
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "_LIB_PATH", os.path.join(ROOT, "paper_2606_02218_amd", "no_such_librollout.so"))
+    with pytest.raises(ImportError, match="no fallback"):
+        _lib.load_library()
+    with pytest.raises(ImportError):
+        _lib.group_advantage(None, None)
+    with pytest.raises(ImportError):
+        _lib.group_filter(None, None)
