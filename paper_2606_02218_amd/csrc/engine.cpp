@@ -709,8 +709,13 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   pol->logit_rows = std::max<int64_t>({S, P, std::min<int64_t>(M, RG_LM_SLICE_ROWS)});
   const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
   pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
-  pol->att_rowchunks = std::max<int64_t>(lim.max_prompt_tokens, S) + ATT_ITEMS_TARGET +
-                       S * (RG_PRE_MAX_SLOTS + ceil_div(lim.max_context, 1024));
+  // (row, context chunk) slots of one attention launch: decode steps (rows <=
+  // S, prefix slots and chunks), and a full activation chunk of prefill or
+  // recompute rows, which splits contexts longer than one chunk's span
+  pol->att_rowchunks = std::max<int64_t>(
+      std::max<int64_t>(lim.max_prompt_tokens, S) + ATT_ITEMS_TARGET +
+          S * (RG_PRE_MAX_SLOTS + ceil_div(lim.max_context, 1024)),
+      M * att_row_chunks((int)std::min<int64_t>(M, INT32_MAX), pol->nkv, lim.max_context));
   pol->hist_cap = lim.max_context;
   struct Piece { void** p; size_t bytes; };
   const int64_t kmax = std::max<int64_t>({d, pol->q_dim, pol->F});
