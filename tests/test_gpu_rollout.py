@@ -12,6 +12,7 @@
   group) agrees with the row-by-row pass within rounding and with the oracle,
   also for a group larger than one prefix workgroup's 128 query rows.
 * temperatures other than 1 (0.7, 1.6): free-running and teacher-forced.
+* prompt lengths at KV page boundaries (1, 15, 16, 17, 32, 33 tokens).
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -114,6 +115,24 @@ def test_temperature_other_than_one(torch, T):
     prompts, L = _case(GQA, 4, [33, 12], [5, 3], 16, (1, 16))
     ref, tok, ln, lp, dump, _ = _run_tf(torch, GQA, wb, prompts, [5, 3], 16, L, 13, temperature=T)
     _check_tf(ref, tok, ln, lp, dump, L)
+
+
+def test_prompt_lengths_at_page_boundaries(torch):
+    # 16-token KV pages: prompts with no full page (1, 15), exactly one or two
+    # (16, 32), and one token past a boundary (17, 33), each with siblings
+    # that share the full pages and copy the partial one; lengths 1..12
+    from oracle.grpo import teacher_forced_logprobs
+    prompts, L = _case(GQA, 8, [1, 15, 16, 17, 32, 33], [3, 2, 4, 1, 2, 3], 12, (1, 12))
+    G = [3, 2, 4, 1, 2, 3]
+    w = make_weights(GQA, 8)
+    ref, tok, ln, lp, dump, pol = _run_tf(torch, GQA, w, prompts, G, 12, L, 31)
+    _check_tf(ref, tok, ln, lp, dump, L)
+    want = teacher_forced_logprobs(oracle_for(GQA, w), prompts, G, ref["tokens"], ref["lengths"])
+    got = _np(pol.recompute_logprobs(prompts_to_device(prompts), G, torch.from_numpy(ref["tokens"]).cuda(),
+                                     torch.from_numpy(ref["lengths"]).cuda()))
+    valid = np.arange(12)[None, :] < ref["lengths"][:, None]
+    assert np.all(got[~valid] == 0)
+    assert float(np.max(np.abs(got[valid] - want[valid]))) <= 2 * LOGIT_TOL
 
 
 def test_tiny_teacher_forced(torch):
