@@ -13,6 +13,7 @@
   also for a group larger than one prefix workgroup's 128 query rows.
 * temperatures other than 1 (0.7, 1.6): free-running and teacher-forced.
 * prompt lengths at KV page boundaries (1, 15, 16, 17, 32, 33 tokens).
+* a decode batch of more than 1024 rows (256 x 256 projection tiles).
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -133,6 +134,23 @@ def test_prompt_lengths_at_page_boundaries(torch):
     valid = np.arange(12)[None, :] < ref["lengths"][:, None]
     assert np.all(got[~valid] == 0)
     assert float(np.max(np.abs(got[valid] - want[valid]))) <= 2 * LOGIT_TOL
+
+
+def test_decode_batch_above_1024_rows(torch):
+    # 100 prompts x 8..16 siblings: decode steps with more than 1024 rows run
+    # every projection on 256 x 256 tiles with the decode epilogues (QKV with
+    # RoPE and KV append, SwiGLU, residual + norm)
+    rng = np.random.default_rng(77)
+    P = 100
+    G = [int(g) for g in rng.integers(8, 17, size=P)]
+    prompts = [rng.integers(0, GQA.vocab - 1, size=int(n)).astype(np.int32) for n in rng.integers(1, 25, size=P)]
+    N = sum(G)
+    assert N > 1024
+    L = rng.integers(1, 6, size=N).astype(np.int32)
+    L[:1100] = 5                                     # the first steps run above 1024 rows
+    w = make_weights(GQA, 9)
+    ref, tok, ln, lp, dump, _ = _run_tf(torch, GQA, w, prompts, G, 5, L, 41)
+    _check_tf(ref, tok, ln, lp, dump, L)
 
 
 def test_tiny_teacher_forced(torch):
