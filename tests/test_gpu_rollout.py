@@ -14,6 +14,7 @@
 * temperatures other than 1 (0.7, 1.6): free-running and teacher-forced.
 * prompt lengths at KV page boundaries (1, 15, 16, 17, 32, 33 tokens).
 * a decode batch of more than 1024 rows (256 x 256 projection tiles).
+* graph replay and direct launches (kernel timing) give bit-identical outputs.
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -151,6 +152,27 @@ def test_decode_batch_above_1024_rows(torch):
     w = make_weights(GQA, 9)
     ref, tok, ln, lp, dump, _ = _run_tf(torch, GQA, w, prompts, G, 5, L, 41)
     _check_tf(ref, tok, ln, lp, dump, L)
+
+
+def test_graph_replay_matches_direct_launches(torch):
+    # decode steps replay captured HIP graphs unless kernels are being timed;
+    # timing every class, or only the attention class, launches them directly
+    # with events around each launch: the outputs must be bit-identical
+    w = make_weights(GQA, 12)
+    prompts, L = _case(GQA, 12, [40, 7, 19], [5, 3, 4], 24, (1, 24))
+    G = [5, 3, 4]
+    pol = make_policy(GQA, w, max_seqs=12, max_prompts=3, max_prompt_tokens=66, max_context=64)
+    dp = prompts_to_device(prompts)
+    base = [_np(x) for x in pol.rollout(dp, G, 24, 17, forced_len=L)]
+    for prof in (True, ["attn"]):
+        got = [_np(x) for x in pol.rollout(dp, G, 24, 17, forced_len=L, profile=prof)]
+        for g, b in zip(got, base):
+            np.testing.assert_array_equal(g, b)
+        times = pol.kernel_times(1)
+        assert times["attn"][1] > 0 and times["attn"][0] > 0
+        if prof is True:
+            assert all(n > 0 for k, (ms, n) in times.items() if k in ("gemm_qkv", "gemm_o", "gemm_gu", "gemm_down",
+                                                                       "gemm_lm", "sample"))
 
 
 def test_tiny_teacher_forced(torch):
