@@ -14,7 +14,8 @@
 * temperatures other than 1 (0.7, 1.6): free-running and teacher-forced.
 * prompt lengths at KV page boundaries (1, 15, 16, 17, 32, 33 tokens).
 * a decode batch of more than 1024 rows (256 x 256 projection tiles).
-* graph replay and direct launches (kernel timing) give bit-identical outputs.
+* graph replay and direct launches (kernel timing) give bit-identical outputs;
+  so does a non-default caller stream.
 * edge cases: length-1 completions, max_new = 1, natural EOS, errors.
 """
 import numpy as np
@@ -173,6 +174,34 @@ def test_graph_replay_matches_direct_launches(torch):
         if prof is True:
             assert all(n > 0 for k, (ms, n) in times.items() if k in ("gemm_qkv", "gemm_o", "gemm_gu", "gemm_down",
                                                                        "gemm_lm", "sample"))
+
+
+def test_side_stream_matches_default_stream(torch):
+    # every entry point launches on the caller's stream (here torch's current
+    # stream inside a side-stream context): same outputs, bit for bit
+    import paper_2606_02218_amd as rg
+    w = make_weights(GQA, 14)
+    prompts, L = _case(GQA, 14, [21, 9], [4, 3], 16, (1, 16))
+    G = [4, 3]
+    pol = make_policy(GQA, w, max_seqs=7, max_prompts=2, max_prompt_tokens=30, max_context=40)
+    dp = prompts_to_device(prompts)
+    base = [_np(x) for x in pol.rollout(dp, G, 16, 23, forced_len=L)]
+    tok0, ln0 = (torch.from_numpy(base[0]).cuda(), torch.from_numpy(base[1]).cuda())
+    rec0 = _np(pol.recompute_logprobs(dp, G, tok0, ln0))
+    r = torch.from_numpy(np.random.default_rng(3).random(7).astype(np.float32)).cuda()
+    Gd = torch.tensor(G, dtype=torch.int32).cuda()
+    adv0 = _np(rg.group_advantage(r, Gd))
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        got = pol.rollout(dp, G, 16, 23, forced_len=L)
+        rec = pol.recompute_logprobs(dp, G, tok0, ln0)
+        adv = rg.group_advantage(r, Gd)
+    side.synchronize()
+    for g, b in zip(got, base):
+        np.testing.assert_array_equal(_np(g), b)
+    np.testing.assert_array_equal(_np(rec), rec0)
+    np.testing.assert_array_equal(_np(adv), adv0)
 
 
 def test_tiny_teacher_forced(torch):
