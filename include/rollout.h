@@ -123,8 +123,9 @@ typedef struct rg_policy rg_policy;  /* opaque: packed weights, KV pool, workspa
                                         shared pages from L2 and is faster at G = 16.     */
 
 #define RG_FLAG_NO_ROW_TILES      8  /* recompute_logprobs: attend row by row instead of by
-                                        tiles of 16 positions of a sequence sharing each
-                                        staged K/V block (a test and measurement aid)     */
+                                        tiles of 32 positions (16 for wide GQA groups) of a
+                                        sequence sharing each staged K/V block (a test and
+                                        measurement aid)                                   */
 
 /* Sampling options.  A NULL rg_sampling* means temperature 1, natural EOS, no
  * flags.  Token t of sequence s is argmax_v fp32(z_v/T) + g_v where g_v is the
