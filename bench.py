@@ -328,6 +328,9 @@ def main():
                     help="only run the static-G vs controller sweep at EB = 64 with T steps per arm and exit")
     ap.add_argument("--group-prefix", action="store_true",
                     help="decode steps attend to each prompt's shared prefix once per group (RG_FLAG_GROUP_PREFIX)")
+    ap.add_argument("--history-out", default="", metavar="PATH",
+                    help="write the last rollout's step history (active rows, groups, prompt tokens per step) "
+                         "and the per-token KV bytes to PATH (.npz) for `prof phases`")
     ap.add_argument("--loss-forward", action="store_true",
                     help="only run the GRPO loss forward (logprob recompute + clipped surrogate) and exit")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
@@ -408,6 +411,10 @@ def main():
     dt = time.perf_counter() - t0
     gen = int(lengths.sum().item()) * 1  # tokens of the last step; every step has the same forced lengths
     hist_a, hist_g, hist_c = pol.step_history()
+    if args.history_out:
+        np.savez(args.history_out, active=np.asarray(hist_a), groups=np.asarray(hist_g), ctx=np.asarray(hist_c),
+                 n_layers=shape.n_layers, kv_bytes_per_token_layer=2 * shape.kv_dim * shape.elem_bytes,
+                 q_bytes_per_row=shape.q_dim * 8)
     assert np.array_equal(lengths.cpu().numpy(), inp.forced_len), "retired lengths differ from the forced lengths"
 
     ms_per_step = dt / args.steps * 1e3

@@ -3,6 +3,7 @@
     python -m paper_2606_02218_amd.prof stats DIR              # per-kernel time table
     python -m paper_2606_02218_amd.prof trace DIR [TOP]        # per kernel and grid size, from kernel_trace.csv
     python -m paper_2606_02218_amd.prof steps DIR              # decode-step time by active-row bucket
+    python -m paper_2606_02218_amd.prof phases DIR HIST.npz    # decode attention by phase of one rollout
     python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
 """
 from __future__ import annotations
@@ -106,6 +107,62 @@ def steps_table(d: str) -> str:
     return "\n".join(out)
 
 
+def phases_table(d: str, hist_path: str) -> str:
+    """Decode attention of one rollout (the trace's only rollout) by phase:
+    steps grouped by their active-row count.  HIST.npz is the step history
+    that `bench.py --history-out` writes.  The first n_layers per-row
+    attention launches attend the prompt rows; after them decode step t owns
+    launches (t-1)*n_layers .. t*n_layers-1, and a merge launch belongs to the
+    attention launch before it.  Algorithmic bytes count each active group's
+    prompt once; wave-read bytes count it once per row (what the per-row
+    pass's waves read, the repeats served by L2)."""
+    import numpy as np
+    h = np.load(hist_path)
+    A, Gr, C = h["active"], h["groups"], h["ctx"]
+    L = int(h["n_layers"])
+    kvb, qb = float(h["kv_bytes_per_token_layer"]), float(h["q_bytes_per_row"])
+    ev = []
+    for f in _find(d, "kernel_trace.csv"):
+        for r in csv.DictReader(open(f)):
+            n = _kname(r)
+            if n in ("k_attention_mfma", "k_attn_merge"):
+                s0 = int(r["Start_Timestamp"])
+                ev.append((s0, int(r["End_Timestamp"]) - s0, n == "k_attn_merge"))
+    ev.sort()
+    att = []
+    for _, dt, is_merge in ev:
+        if is_merge:
+            if att:
+                att[-1][1] += dt
+        else:
+            att.append([dt, 0])
+    bins = [(257, 1 << 30), (129, 256), (65, 128), (33, 64), (17, 32), (1, 16)]
+    acc = {b: [0, 0.0, 0.0, 0.0, 0.0] for b in bins}
+    used = 0
+    for i, (dt, dm) in enumerate(att[L:]):
+        t = 1 + i // L
+        if t >= len(A) or int(A[t]) == 0:
+            break
+        M, g = int(A[t]), int(Gr[t])
+        alg = (float(C[t]) / M * g + M * t) * kvb + M * qb
+        wave = (float(C[t]) + M * t) * kvb + M * qb
+        a = acc[next(b for b in bins if b[0] <= M <= b[1])]
+        a[0] += 1; a[1] += dt; a[2] += dm; a[3] += alg; a[4] += wave
+        used += 1
+    out = [f"decode attention launches {len(att) - L} (after {L} prompt-row launches), {used} matched to steps",
+           f"{'rows':>9s} {'launches':>9s} {'attn_ms':>8s} {'merge_ms':>9s} {'us/launch':>10s} {'alg_MB':>8s} "
+           f"{'alg_TB/s':>9s} {'wave_TB/s':>10s}"]
+    ta = tm = 0.0
+    for (lo, hi), (n, dt, dm, alg, wave) in acc.items():
+        if n:
+            ta += dt; tm += dm
+            label = f"{lo}+" if hi == 1 << 30 else f"{lo}-{hi}"
+            out.append(f"{label:>9s} {n:9d} {dt / 1e6:8.1f} {dm / 1e6:9.1f} {dt / n / 1e3:10.2f} "
+                       f"{alg / n / 1e6:8.1f} {alg / dt / 1e3:9.2f} {wave / dt / 1e3:10.2f}")
+    out.append(f"total: attention {ta / 1e6:.1f} ms, merge {tm / 1e6:.1f} ms")
+    return "\n".join(out)
+
+
 def counter_table(d: str, regex: str) -> str:
     pat = re.compile(regex)
     acc = collections.defaultdict(lambda: [0, 0.0])
@@ -131,6 +188,8 @@ if __name__ == "__main__":
         print(trace_table(sys.argv[2], int(sys.argv[3]) if len(sys.argv) > 3 else 60))
     elif len(sys.argv) >= 3 and sys.argv[1] == "steps":
         print(steps_table(sys.argv[2]))
+    elif len(sys.argv) >= 4 and sys.argv[1] == "phases":
+        print(phases_table(sys.argv[2], sys.argv[3]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
         print(counter_table(sys.argv[2], sys.argv[3]))
     else:
