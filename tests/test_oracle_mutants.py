@@ -3,15 +3,19 @@ function's source, applies one plausible slip (a max for a min, swapped clip
 bounds, a dropped normalisation or sign, a mean or variance divided by the
 wrong count, a dropped epsilon), runs the mutant through the committed pins of
 that function, and requires at least one pin to reject it.  The unmutated
-functions pass every pin."""
+functions pass every pin.  Covered: the clipped surrogate, the group-relative
+advantage, and the controller's straggler statistics, dual and posterior
+update and neighbourhood choice."""
 import inspect
 
 import pytest
 
 import oracle.advantage as oracle_advantage
 import oracle.grpo as oracle_grpo
+import oracle.sagc as oracle_sagc
 import test_oracle_grpo as grpo_pins
 import test_oracle_rollout as rollout_pins
+import test_oracle_sagc as sagc_pins
 
 
 def _mutant(fn, old, new):
@@ -59,9 +63,31 @@ ADVANTAGE_SLIPS = {
 }
 
 
+SAGC_PINS = [sagc_pins.test_group_stats_worked_examples, sagc_pins.test_group_stats_match_numpy,
+             sagc_pins.test_dual_and_posterior_worked_example, sagc_pins.test_choice_rules] + \
+    [lambda s=s: sagc_pins.test_closed_loop_separates_arms(s) for s in (0, 1)]
+
+SAGC_SLIPS = {
+    "stats_even_median_upper": ("group_stats", "(seg[g // 2 - 1] + seg[g // 2]) / 2.0", "float(seg[g // 2])"),
+    "stats_tau_inclusive": ("group_stats", "1.0 if R > tau else 0.0", "1.0 if R >= tau else 0.0"),
+    "stats_max_is_first": ("group_stats", "lmax = seg[-1]", "lmax = seg[0]"),
+    "stats_unsorted": ("group_stats", "seg = sorted(int(v) for v in lengths[off:off + g])",
+                       "seg = [int(v) for v in lengths[off:off + g]]"),
+    "dual_step_sign": ("sagc_step", "st.lam + cfg.eta * (s_bar - cfg.delta)", "st.lam - cfg.eta * (s_bar - cfg.delta)"),
+    "dual_not_projected": ("sagc_step", "max(0.0, st.lam + cfg.eta * (s_bar - cfg.delta))",
+                           "(st.lam + cfg.eta * (s_bar - cfg.delta))"),
+    "posterior_counts_swapped": ("sagc_step", "cfg.gamma * st.alpha[i] + s_bar", "cfg.gamma * st.alpha[i] + (1.0 - s_bar)"),
+    "posterior_not_discounted": ("sagc_step", "st.beta[i] = cfg.gamma * st.beta[i]", "st.beta[i] = st.beta[i]"),
+    "choice_ties_to_larger": ("sagc_choose", "scores[i] > scores[best]", "scores[i] >= scores[best]"),
+    "choice_penalty_sign": ("sagc_choose", "- lam * samples[i]", "+ lam * samples[i]"),
+    "choice_whole_range": ("sagc_choose", "(g_index - 1, g_index, g_index + 1)", "range(k)"),
+}
+
+
 def test_unmutated_oracle_passes_every_pin():
     assert not _rejected(SURROGATE_PINS)
     assert not _rejected(ADVANTAGE_PINS)
+    assert not _rejected(SAGC_PINS)
 
 
 @pytest.mark.parametrize("name", sorted(SURROGATE_SLIPS))
@@ -77,3 +103,11 @@ def test_advantage_slip_is_rejected(name, monkeypatch):
     monkeypatch.setattr(rollout_pins, "group_advantage", bad)
     monkeypatch.setattr(grpo_pins, "group_advantage", bad)
     assert _rejected(ADVANTAGE_PINS), name
+
+
+@pytest.mark.parametrize("name", sorted(SAGC_SLIPS))
+def test_controller_slip_is_rejected(name, monkeypatch):
+    fn_name, old, new = SAGC_SLIPS[name]
+    bad = _mutant(getattr(oracle_sagc, fn_name), old, new)
+    monkeypatch.setattr(oracle_sagc, fn_name, bad)
+    assert _rejected(SAGC_PINS), name
