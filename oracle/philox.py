@@ -79,9 +79,14 @@ def uniforms_from_bits(x: np.ndarray) -> np.ndarray:
     return ((2.0 * k + 1.0) * 2.0 ** -24).astype(np.float32)
 
 
-def gumbel_noise(seed: int, t: int, s: int, vocab: int) -> np.ndarray:
-    """fp32 [vocab] standard Gumbel variates g = -log(-log(u)), in fp32."""
-    u = uniforms_from_bits(gumbel_uniform_bits(seed, t, s, vocab))
+def gumbel_noise(seed: int, t: int, s, vocab: int) -> np.ndarray:
+    """fp32 [vocab] standard Gumbel variates g = -log(-log(u)), in fp32, for
+    sequence s at decode step t; an array of sequence ids gives
+    [len(s), vocab], row i for sequence s[i]."""
+    if np.ndim(s) == 0:
+        u = uniforms_from_bits(gumbel_uniform_bits(seed, t, int(s), vocab))
+    else:
+        u = uniforms_from_bits(gumbel_uniform_bits_batch(seed, t, s, vocab))
     return -np.log(-np.log(u))
 
 

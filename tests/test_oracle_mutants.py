@@ -4,18 +4,28 @@ bounds, a dropped normalisation or sign, a mean or variance divided by the
 wrong count, a dropped epsilon), runs the mutant through the committed pins of
 that function, and requires at least one pin to reject it.  The unmutated
 functions pass every pin.  Covered: the clipped surrogate, the group-relative
-advantage, and the controller's straggler statistics, dual and posterior
-update and neighbourhood choice."""
+advantage, the controller's straggler statistics, dual and posterior update
+and neighbourhood choice, and the sampler's noise, uniform mapping, bit
+layout, temperature, forced EOS, log-probability and tie rule."""
+import importlib
 import inspect
 
 import pytest
 
 import oracle.advantage as oracle_advantage
 import oracle.grpo as oracle_grpo
+import oracle.philox as oracle_philox
 import oracle.sagc as oracle_sagc
+import oracle.sampling as oracle_sampling
 import test_oracle_grpo as grpo_pins
+import test_oracle_philox as philox_pins
 import test_oracle_rollout as rollout_pins
 import test_oracle_sagc as sagc_pins
+from oracle.model import OracleModel
+from workload import make_inputs, make_weights
+
+# the package re-exports the function `rollout` under the submodule's name
+oracle_rollout = importlib.import_module("oracle.rollout")
 
 
 def _mutant(fn, old, new):
@@ -111,3 +121,47 @@ def test_controller_slip_is_rejected(name, monkeypatch):
     bad = _mutant(getattr(oracle_sagc, fn_name), old, new)
     monkeypatch.setattr(oracle_sagc, fn_name, bad)
     assert _rejected(SAGC_PINS), name
+
+
+def _tiny():
+    return OracleModel(grpo_pins.TINY.shape, make_weights(grpo_pins.TINY.shape, 0)), make_inputs(grpo_pins.TINY, 0)
+
+
+SAMPLING_PINS = [philox_pins.test_gumbel_bits_layout, philox_pins.test_uniform_mapping_endpoints_and_exactness,
+                 philox_pins.test_sample_token_forced_eos_and_logprob, philox_pins.test_sample_token_tie_goes_to_lowest_id,
+                 lambda: grpo_pins.test_recompute_equals_rollout_logprobs(_tiny(), 0.7)] + \
+    [lambda T=T: philox_pins.test_sample_token_frequencies_match_softmax(T) for T in (1.0, 0.7)] + \
+    [lambda T=T: philox_pins.test_gumbel_max_frequencies_match_softmax(T) for T in (1.0, 0.7)]
+
+# (module, function, old text, new text)
+SAMPLING_SLIPS = {
+    "noise_sign": (oracle_philox, "gumbel_noise", "return -np.log(-np.log(u))", "return np.log(-np.log(u))"),
+    "uniform_reaches_one": (oracle_philox, "uniforms_from_bits", "((2.0 * k + 1.0) * 2.0 ** -24)",
+                            "((k + 1.0) * 2.0 ** -23)"),
+    "high_half_lost": (oracle_philox, "gumbel_uniform_bits", "halves[:, 1::2] = w >> _S32",
+                       "halves[:, 1::2] = w & _M32"),
+    "temperature_multiplies": (oracle_sampling, "sample_token", "z.astype(np.float32) / np.float32(temperature)",
+                               "z.astype(np.float32) * np.float32(temperature)"),
+    "logprob_ignores_temperature": (oracle_sampling, "sample_token", "zt = z / float(temperature)", "zt = z"),
+    "forced_eos_one_late": (oracle_sampling, "sample_token", "t == int(forced_len) - 1", "t == int(forced_len)"),
+    "eos_not_masked": (oracle_sampling, "sample_token", "score[eos_id] = -np.inf", "score[eos_id] = score[eos_id]"),
+    "logprob_unnormalised": (oracle_sampling, "sample_token", "float(zt[y] - lse)", "float(zt[y])"),
+    "ties_to_highest_id": (oracle_sampling, "sample_token", "int(np.argmax(score))",
+                           "int(len(score) - 1 - np.argmax(score[::-1]))"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SAMPLING_SLIPS))
+def test_sampling_slip_is_rejected(name, monkeypatch):
+    mod, fn_name, old, new = SAMPLING_SLIPS[name]
+    bad = _mutant(getattr(mod, fn_name), old, new)
+    monkeypatch.setattr(mod, fn_name, bad)
+    # every module that imported the function by name
+    for m in (oracle_sampling, oracle_rollout, philox_pins, grpo_pins):
+        if getattr(m, fn_name, None) is not None and m is not mod:
+            monkeypatch.setattr(m, fn_name, bad)
+    assert _rejected(SAMPLING_PINS), name
+
+
+def test_unmutated_sampler_passes_every_pin():
+    assert not _rejected(SAMPLING_PINS)

@@ -91,8 +91,7 @@ def _gumbel_max_counts(z, n_draws, seed=3, T=1.0):
     zs = (np.asarray(z, np.float32) / np.float32(T)).astype(np.float32)
     for c0 in range(0, n_draws, chunk):
         s = np.arange(c0, min(n_draws, c0 + chunk))
-        u = uniforms_from_bits(gumbel_uniform_bits_batch(seed, 0, s, V))
-        g = -np.log(-np.log(u))
+        g = gumbel_noise(seed, 0, s, V)            # the oracle's own noise, one row per draw
         y = np.argmax(zs[None, :] + g, axis=1)
         counts += np.bincount(y, minlength=V)
     return counts
@@ -104,6 +103,17 @@ def test_gumbel_max_frequencies_match_softmax(T):
     z = rng.normal(0, 1.5, size=16)
     n = 1_000_000
     counts = _gumbel_max_counts(z, n, T=T)
+    p = np.exp(z / T - np.max(z / T)); p /= p.sum()
+    assert stats.chisquare(counts, n * p).pvalue > 1e-3
+
+
+@pytest.mark.parametrize("T", [1.0, 0.7])
+def test_sample_token_frequencies_match_softmax(T):
+    # the oracle's full sampling decision (scaling by T, noise, argmax), one
+    # call per draw: 20,000 draws on 6 tokens against softmax(z/T)
+    z = np.array([0.3, -1.1, 1.4, 0.0, -0.4, 0.9])
+    n = 20_000
+    counts = np.bincount([sample_token(z, 9, 0, s, len(z) - 1, T)[0] for s in range(n)], minlength=len(z))
     p = np.exp(z / T - np.max(z / T)); p /= p.sum()
     assert stats.chisquare(counts, n * p).pvalue > 1e-3
 
