@@ -5,8 +5,9 @@ wrong count, a dropped epsilon), runs the mutant through the committed pins of
 that function, and requires at least one pin to reject it.  The unmutated
 functions pass every pin.  Covered: the clipped surrogate, the group-relative
 advantage, the controller's straggler statistics, dual and posterior update
-and neighbourhood choice, and the sampler's noise, uniform mapping, bit
-layout, temperature, forced EOS, log-probability and tie rule."""
+and neighbourhood choice, the sampler's noise, uniform mapping, bit layout,
+temperature, forced EOS, log-probability and tie rule, and the teacher-forced
+log-probabilities of the loss forward."""
 import importlib
 import inspect
 
@@ -165,3 +166,23 @@ def test_sampling_slip_is_rejected(name, monkeypatch):
 
 def test_unmutated_sampler_passes_every_pin():
     assert not _rejected(SAMPLING_PINS)
+
+
+RECOMPUTE_PINS = [lambda T=T: grpo_pins.test_recompute_equals_rollout_logprobs(_tiny(), T) for T in (1.0, 0.7)]
+
+RECOMPUTE_SLIPS = {
+    "logits_row_one_late": ("zt = z[Lp - 1 + t] / float(temperature)", "zt = z[min(Lp + t, len(z) - 1)] / float(temperature)"),
+    "temperature_dropped": ("zt = z[Lp - 1 + t] / float(temperature)", "zt = z[Lp - 1 + t]"),
+    "unnormalised": ("out[s, t] = zt[y[t]] - logsumexp(zt)", "out[s, t] = zt[y[t]]"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(RECOMPUTE_SLIPS))
+def test_recompute_slip_is_rejected(name, monkeypatch):
+    bad = _mutant(oracle_grpo.teacher_forced_logprobs, *RECOMPUTE_SLIPS[name])
+    monkeypatch.setattr(grpo_pins, "teacher_forced_logprobs", bad)
+    assert _rejected(RECOMPUTE_PINS), name
+
+
+def test_unmutated_recompute_passes_its_pins():
+    assert not _rejected(RECOMPUTE_PINS)
