@@ -709,6 +709,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
   pol->logit_rows = std::max<int64_t>({S, P, std::min<int64_t>(M, RG_LM_SLICE_ROWS)});
   const int64_t maxN = std::max<int64_t>({pol->qkv_n, 2LL * pol->F, d});
   pol->cpart_elems = std::max(M * maxN, (int64_t)RG_SPLIT_MAX * S * maxN);
+  // fp32 models run every projection through the partial buffer, the lm head
+  // too: up to max(M, logit_rows) rows of the vocabulary
+  if (pol->dtype != RG_DTYPE_BF16)
+    pol->cpart_elems = std::max(pol->cpart_elems, std::max(M, pol->logit_rows) * (int64_t)pol->V);
   // (row, context chunk) slots of one attention launch: decode steps (rows <=
   // S, prefix slots and chunks), and a full activation chunk of prefill or
   // recompute rows, which splits contexts longer than one chunk's span

@@ -16,7 +16,9 @@
 * a decode batch of more than 1024 rows (256 x 256 projection tiles).
 * graph replay and direct launches (kernel timing) give bit-identical outputs;
   so does a non-default caller stream.
-* edge cases: length-1 completions, max_new = 1, natural EOS, errors.
+* edge cases: length-1 completions, max_new = 1, natural EOS, errors; an fp32
+  model whose vocabulary is wider than every projection (its lm head runs
+  through the GEMM partial buffer at the 16-row decode bucket).
 """
 import numpy as np
 import pytest
@@ -31,6 +33,7 @@ pytestmark = pytest.mark.gpu
 GQA = ModelShape(2, 256, 12, 2, 128, 512, 2048, 1e6, dtype="bf16")
 GPT2S = get_config("gpt2s").shape
 NAT = ModelShape(2, 64, 2, 2, 32, 128, 16, 1e4, dtype="f32")   # 16-token vocab: EOS comes naturally
+WIDE_V = ModelShape(1, 64, 4, 1, 32, 128, 2000, 1e4, dtype="f32")   # vocabulary wider than every projection
 
 
 @pytest.fixture(scope="module")
@@ -211,6 +214,16 @@ def test_tiny_teacher_forced(torch):
     ref, tok, ln, lp, dump, _ = _run_tf(torch, wl.shape, w, prompts, [4, 3, 2], 32, L, 5)
     worst, _ = _check_tf(ref, tok, ln, lp, dump, L)
     assert worst < 1e-4   # fp32 model: only accumulation-order differences
+
+
+def test_fp32_vocabulary_wider_than_projections(torch):
+    # fp32 models run the lm head through the GEMM partial buffer: one
+    # sequence decodes in the 16-row bucket, which needs 16 x V elements
+    w = make_weights(WIDE_V, 9)
+    prompts, L = _case(WIDE_V, 9, [12], [1], 3, (1, 3))
+    ref, tok, ln, lp, dump, _ = _run_tf(torch, WIDE_V, w, prompts, [1], 3, L, 34)
+    worst, _ = _check_tf(ref, tok, ln, lp, dump, L)
+    assert worst < 1e-4
 
 
 def test_gqa_bf16_teacher_forced(torch):
