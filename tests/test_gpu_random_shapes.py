@@ -3,8 +3,10 @@
 Each case draws a model (bf16 or fp32; head_dim 32/64/128; 1, 2 or 4 kv
 heads with 1..8 query heads each; d_model, FFN and vocabulary sizes; 1..3
 layers; RoPE theta 1e4 or 1e6), a batch (1..4 ragged prompts, G per prompt,
-forced lengths up to max_new), a temperature (1, 0.7 or 1.3) and whether the
-siblings share their prompt's pages, then checks:
+forced lengths up to max_new), a temperature (1, 0.7 or 1.3), whether the
+siblings share their prompt's pages, whether bf16 decode steps take the group
+prefix pass, and whether the recompute attends by row tiles or by rows, then
+checks:
 
 * the rollout teacher-forced on the oracle's tokens: every logit within 1e-2
   (bf16) / 1e-4 (fp32) of the oracle's, log-probabilities within twice that,
@@ -57,7 +59,8 @@ def draw_case(i):
     prompts = [r.integers(0, V - 1, size=n).astype(np.int32) for n in plens]
     T = float(r.choice([1.0, 0.7, 1.3]))
     share = bool(r.random() < 0.8)
-    return shape, prompts, G, max_new, lengths, T, share
+    modes = dict(group_prefix=bool(r.random() < 0.3), row_tiles=bool(r.random() < 0.7))
+    return shape, prompts, G, max_new, lengths, T, share, modes
 
 
 @pytest.mark.timeout(300)
@@ -65,9 +68,9 @@ def draw_case(i):
 def test_random_shape_against_oracle(i):
     import torch
     assert torch.cuda.is_available()
-    shape, prompts, G, max_new, L, T, share = draw_case(i)
+    shape, prompts, G, max_new, L, T, share, modes = draw_case(i)
     print(f"random case {i}: {shape}, prompts {[len(p) for p in prompts]}, G {G}, max_new {max_new}, T {T}, "
-          f"shared pages {share}", flush=True)
+          f"shared pages {share}, {modes}", flush=True)
     w = make_weights(shape, 5000 + i)
     model = oracle_for(shape, w)
     ref = oracle_rollout(model, prompts, G, max_new, 77 + i, L, record_steps=max_new, temperature=T)
@@ -76,7 +79,7 @@ def test_random_shape_against_oracle(i):
     ft = torch.from_numpy(ref["tokens"]).cuda()
     dp = prompts_to_device(prompts)
     tok, ln, lp, dump = pol.rollout(dp, G, max_new, 77 + i, forced_len=L, force_tokens=ft, dump_steps=max_new,
-                                    temperature=T, share_prefix=share)
+                                    temperature=T, share_prefix=share, group_prefix_pass=modes["group_prefix"])
     torch.cuda.synchronize()
     tok, ln, lp, dump = tok.cpu().numpy(), ln.cpu().numpy(), lp.cpu().numpy(), dump.cpu().numpy()
     tol = 1e-2 if shape.dtype == "bf16" else 1e-4
@@ -88,13 +91,14 @@ def test_random_shape_against_oracle(i):
             assert abs(float(lp[s, t]) - float(ref["logprobs"][s, t])) <= 2 * tol, (s, t)
             if tok[s, t] != ref["tokens"][s, t]:
                 assert ref["margins"][s, t] < MARGIN_TOL, (s, t, ref["margins"][s, t])
-    tok2, ln2, lp2 = pol.rollout(dp, G, max_new, 77 + i, forced_len=L, temperature=T, share_prefix=share)
+    tok2, ln2, lp2 = pol.rollout(dp, G, max_new, 77 + i, forced_len=L, temperature=T, share_prefix=share,
+                                 group_prefix_pass=modes["group_prefix"])
     tok2, ln2, lp2 = tok2.cpu().numpy(), ln2.cpu().numpy(), lp2.cpu().numpy()
     check_structure(tok2, ln2, lp2, shape.eos_id, max_new, L)
     compare_free_running(tok2, lp2, ref, ln2, lp_tol=2 * tol)
     want = teacher_forced_logprobs(model, prompts, G, ref["tokens"], ref["lengths"], T)
     got = pol.recompute_logprobs(dp, G, ft, torch.from_numpy(ref["lengths"]).cuda(), temperature=T,
-                                 share_prefix=share).cpu().numpy()
+                                 share_prefix=share, row_tiles=modes["row_tiles"]).cpu().numpy()
     valid = np.arange(max_new)[None, :] < ref["lengths"][:, None]
     assert np.all(got[~valid] == 0)
     assert float(np.max(np.abs(got[valid] - want[valid]))) <= 2 * tol
