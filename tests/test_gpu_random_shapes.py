@@ -18,7 +18,9 @@ checks:
 
 The default run takes 16 small cases; RG_SWEEP_CASES=N sets the count and
 RG_SWEEP_BIG=1 draws larger models and batches (d_model up to 1536, FFN up to
-6144, vocabularies up to 32000, prompts up to 600 tokens, up to 16 siblings).
+6144, vocabularies up to 32000, prompts up to 600 tokens, up to 16 siblings);
+RG_SWEEP_LONG=1 draws small models with prompts of 300..2500 tokens, so decode
+rows are cut into many context chunks and merged.
 """
 import os
 
@@ -33,11 +35,12 @@ from rg_helpers import oracle_for, make_policy, prompts_to_device, compare_free_
 pytestmark = pytest.mark.gpu
 
 BIG = os.environ.get("RG_SWEEP_BIG") == "1"
+LONG = os.environ.get("RG_SWEEP_LONG") == "1"
 N_CASES = int(os.environ.get("RG_SWEEP_CASES", "16"))
 
 
 def draw_case(i):
-    r = np.random.default_rng((7000 if BIG else 1000) + i)
+    r = np.random.default_rng((9000 if LONG else (7000 if BIG else 1000)) + i)
     bf = r.random() < 0.8
     hd = int(r.choice([64, 128])) if bf else int(r.choice([32, 64, 128]))
     nkv = int(r.choice([1, 2, 4]))
@@ -48,12 +51,12 @@ def draw_case(i):
     d = 64 * int(r.integers(2, 25 if BIG else 9))
     ffn = 64 * int(r.integers(2, 97 if BIG else 13))
     V = 16 * int(r.integers(32, 2001 if BIG else 257))
-    L = int(r.integers(1, 3 if BIG else 4))
+    L = int(r.integers(1, 3 if (BIG or LONG) else 4))
     theta = float(r.choice([1e4, 1e6]))
     shape = ModelShape(L, d, nq, nkv, hd, ffn, V, theta, dtype="bf16" if bf else "f32")
     P = int(r.integers(1, 5))
-    plens = [int(r.integers(1, 601 if BIG else 81)) for _ in range(P)]
-    G = [int(r.integers(1, 17 if BIG else 7)) for _ in range(P)]
+    plens = [int(r.integers(300, 2501) if LONG else r.integers(1, 601 if BIG else 81)) for _ in range(P)]
+    G = [int(r.integers(1, 17 if BIG else (4 if LONG else 7))) for _ in range(P)]
     max_new = int(r.integers(1, 49 if BIG else 25))
     lengths = r.integers(1, max_new + 1, size=sum(G)).astype(np.int32)
     prompts = [r.integers(0, V - 1, size=n).astype(np.int32) for n in plens]
