@@ -972,8 +972,9 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
   int* d_chunk = pol->state + 11;
   int* d_slice = pol->state + 12;
   int* d_tiles = pol->state + 13;
-  // bf16 models: attention by row tiles (16 positions of a sequence share
-  // each staged K/V block); RG_FLAG_NO_ROW_TILES keeps the per-row pass
+  // bf16 models: attention by row tiles (32 positions of a sequence, 16 when
+  // more than 6 query heads share a kv head, share each staged K/V block);
+  // RG_FLAG_NO_ROW_TILES keeps the per-row pass
   const bool use_tiles = pol->dtype == RG_DTYPE_BF16 && !(flags & RG_FLAG_NO_ROW_TILES) &&
                          pol->nq / pol->nkv <= 8 && ctx_all <= 16384;
   const int tile_rows = att_tile_rows(pol->nq, pol->nkv);

@@ -94,8 +94,8 @@ def test_recompute_gqa_bf16_many_chunks(torch):
 
 
 def test_recompute_row_tiles_match_row_pass(torch):
-    """The row-tile attention (16 positions of a sequence per staged K/V
-    block) against the per-row pass: both within the oracle tolerance and
+    """The row-tile attention (32 positions of a sequence per staged K/V
+    block at 6 query heads per kv head) against the per-row pass: both within the oracle tolerance and
     within 2e-3 of each other; a long completion spans many tiles and chunks,
     sequences of length 1 and 2 give empty and one-row tiles."""
     w = make_weights(GQA, 6)
