@@ -69,6 +69,17 @@ def decode_bytes_total(shape, hist_active, hist_groups, hist_ctx):
     return tot
 
 
+def prefill_flops(shape, plens):
+    """Algorithmic flops of the prefill (one multiply-add = 2 flops): every
+    prompt token through every layer's matrices, causal attention (QK^T and
+    PV: query i of a prompt scores i + 1 positions), and the lm head at each
+    prompt's last position."""
+    L, d, V, hd, nq = shape.n_layers, shape.d_model, shape.vocab, shape.head_dim, shape.n_q_heads
+    n = np.asarray(plens, np.float64)
+    return (2.0 * L * shape.matrix_params_per_layer() * n.sum() + 2.0 * L * nq * hd * float(np.sum(n * (n + 1)))
+            + 2.0 * V * d * len(n))
+
+
 def cpu_baseline(wl, weights, inputs, n_steps: int):
     """The oracle on the host: prefill of prompt 0 plus its G siblings for
     n_steps decode steps (a bounded sample of the same workload)."""
@@ -315,6 +326,56 @@ def measured_traffic(workload, kernel):
     return int(kv["traffic_bytes_per_launch"])
 
 
+def ceilings():
+    """Measured ceilings beside the spec peaks: HBM streaming (a device copy
+    and a read-only reduction over 2 GiB) and bf16 dense MFMA (the platform
+    GEMM, hipBLASLt through torch.matmul, on a large square product and on
+    the 1.5B projection shapes at 16384 and 512 rows).  Best of 10 timed
+    repeats after 3 warmups, HIP events on torch's stream.  Prints one JSON
+    line."""
+    import torch
+
+    def best_ms(fn, reps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        out = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            out.append(e0.elapsed_time(e1))
+        return min(out)
+
+    res = {"hbm_peak_spec_GBps": HBM_PEAK / 1e9, "mfma_bf16_peak_spec_TFLOPs": MFMA_BF16_PEAK / 1e12}
+    n = 1 << 29                                       # 2 GiB of fp32
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    ms = best_ms(lambda: b.copy_(a))
+    res["copy_2GiB"] = {"ms": round(ms, 3), "GBps": round(2 * 4 * n / ms / 1e6, 1)}
+    ms = best_ms(lambda: a.sum())
+    res["read_sum_2GiB"] = {"ms": round(ms, 3), "GBps": round(4 * n / ms / 1e6, 1)}
+    del a, b
+    g = {}
+    shapes = {"square_8192": (8192, 8192, 8192)}
+    for rows in (16384, 512):
+        shapes.update({f"gate_up_{rows}": (rows, 17920, 1536), f"down_{rows}": (rows, 1536, 8960),
+                       f"qkv_{rows}": (rows, 2048, 1536)})
+    for name, (m, nn, k) in shapes.items():
+        x = torch.randn(m, k, device="cuda").to(torch.bfloat16)
+        w = torch.randn(nn, k, device="cuda").to(torch.bfloat16)
+        wt = w.t()
+        ms = best_ms(lambda: torch.matmul(x, wt))
+        fl = 2.0 * m * nn * k
+        g[name] = {"m_n_k": [m, nn, k], "ms": round(ms, 4), "TFLOPs": round(fl / ms / 1e9, 1),
+                   "frac_of_spec": round(fl / ms / 1e3 / MFMA_BF16_PEAK, 4)}
+        del x, w, wt
+    res["bf16_gemm_torch_matmul"] = g
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -335,7 +396,12 @@ def main():
                     help="only run the GRPO loss forward (logprob recompute + clipped surrogate) and exit")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="only measure the HBM copy / read and bf16 GEMM ceilings and exit")
     args = ap.parse_args()
+    if args.ceilings:
+        ceilings()
+        return
     if args.copy_calib:
         import torch
         n = args.copy_calib * (1 << 20) // 4
@@ -398,9 +464,13 @@ def main():
         dom = "attn"
     torch.cuda.synchronize()
     kt = {}
+    phase = [0.0, 0.0]
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(args.warmup + i, [dom] if profile else False)
+        pf, dc = pol.phase_times()
+        phase[0] += pf
+        phase[1] += dc
         if profile:
             ms, n = pol.kernel_times(1)[dom]
             a = kt.setdefault(dom, [0.0, 0])
@@ -429,6 +499,22 @@ def main():
                       "generated_tokens": gen, "decode_steps": int(len(hist_a)),
                       "group_prefix_pass": bool(args.group_prefix)},
            "group_step_s": round(ms_per_step / 1e3, 4)}
+    # prefill (set-up, prompt tokens through the decoder, last-position lm
+    # head, sibling fork) and decode on the device timeline, timed steps
+    pf_s, dc_s = phase[0] / args.steps / 1e3, phase[1] / args.steps / 1e3
+    F = prefill_flops(shape, [wl.prompt_len] * wl.n_prompts)
+    res["prefill_ms"] = round(pf_s * 1e3, 2)
+    res["decode_s"] = round(dc_s, 4)
+    res["roofline_prefill"] = {"bound": "mfma", "achieved": round(F / pf_s / 1e12, 1), "peak": MFMA_BF16_PEAK / 1e12,
+                               "unit": "TFLOP/s", "frac": round(F / pf_s / MFMA_BF16_PEAK, 4),
+                               "issued_frac": round(2 * F / pf_s / MFMA_BF16_PEAK, 4), "alg_flops": F,
+                               "note": "each fp32 activation enters bf16 MFMA as hi + lo planes: two MFMAs per "
+                                       "product, so the algorithmic fraction is at most half the issued one"}
+    dec_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
+    res["roofline_decode"] = {"bound": "hbm", "achieved": round(dec_b / dc_s / 1e9, 1), "peak": HBM_PEAK / 1e9,
+                              "unit": "GB/s", "frac": round(dec_b / dc_s / HBM_PEAK, 4), "alg_bytes": dec_b,
+                              "note": "whole decode: weights once per step, each active group's prompt KV once, "
+                                      "each row's generated KV and its KV write, over the decode device time"}
     if breakdown:
         res["kernel_ms_breakdown_untimed_step"] = {k: round(v[0], 1) for k, v in
                                                    sorted(breakdown.items(), key=lambda kv: -kv[1][0]) if v[1]}

@@ -298,6 +298,24 @@ int rg_gumbel_bits(uint64_t seed, int32_t t, int32_t s, int32_t vocab, uint32_t*
 int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t* active,
                     int32_t* groups, int64_t* ctx);
 
+/* Device-timeline split of the last successful rollout_group call, from HIP
+ * events the call records on its stream: *prefill_ms from the start of the
+ * prefill to the end of the sibling fork (set-up, every prompt token through
+ * the decoder, the prompts' last-position lm head, page copies), *decode_ms
+ * from there to the last decode step (step 0's sampling included).  Either
+ * pointer may be NULL.  RG_EINVAL when no rollout_group call has completed. */
+int rg_phase_times(const rg_policy* pol, double* prefill_ms, double* decode_ms);
+
+/* Context chunks per row of a decode step's attention: for `rows` active
+ * sequences (rounded up to the step's row bucket: 16, 32, 64, 128, 256, 384,
+ * then multiples of 256), `n_kv` kv heads and the rollout's longest context
+ * `ctx_max` (longest prompt + max_new).  Every row's context is cut into that
+ * many chunks of at least 128 tokens (fewer when the context is shorter), each
+ * chunk's partial softmax is written out and a merge kernel combines them
+ * (more than one chunk).  A test and measurement aid; RG_EINVAL (< 0) for a
+ * non-positive argument. */
+int32_t rg_decode_attention_chunks(int32_t rows, int32_t n_kv, int32_t ctx_max);
+
 /* Kernel classes timed under RG_FLAG_PROFILE. */
 #define RG_K_EMBED      0
 #define RG_K_RMSNORM    1

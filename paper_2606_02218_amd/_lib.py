@@ -21,21 +21,31 @@ KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge"
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
            "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
            "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter",
-           "recompute_logprobs", "grpo_surrogate"]
+           "recompute_logprobs", "grpo_surrogate", "rg_decode_attention_chunks", "rg_phase_times"]
 SAGC_MAX_SIZES = 8
 
 
 def _pack_prompts(prompts):
     """A device int32 [P, Lp] tensor or a list of 1-D ones -> (packed, lengths)."""
     import torch
-    if isinstance(prompts, torch.Tensor) and prompts.dim() == 2:
-        plen = [prompts.shape[1]] * prompts.shape[0]
-        packed = prompts.contiguous().view(-1)
+    if isinstance(prompts, torch.Tensor):
+        _dev("prompts", prompts, torch.int32, ndim=2)
+        if prompts.shape[0] < 1 or prompts.shape[1] < 1:
+            raise ValueError("prompts must hold at least one prompt of at least one token")
+        plen = [int(prompts.shape[1])] * int(prompts.shape[0])
+        packed = prompts.view(-1)
     else:
+        prompts = list(prompts)
+        if not prompts:
+            raise ValueError("prompts must hold at least one prompt")
+        for i, p in enumerate(prompts):
+            _dev(f"prompts[{i}]", p, torch.int32, ndim=1)
+            if p.numel() < 1:
+                raise ValueError(f"prompts[{i}] is empty")
+        if len({p.device for p in prompts}) > 1:
+            raise TypeError("prompts must all be in GPU memory")
         plen = [int(p.numel()) for p in prompts]
-        packed = torch.cat([p.view(-1) for p in prompts])
-    if packed.dtype != torch.int32 or packed.device.type != "cuda":
-        raise TypeError("prompts must be int32 tensors on the GPU")
+        packed = torch.cat(prompts)
     return packed, plen
 
 
@@ -117,6 +127,9 @@ def load_library():
                                        C.c_void_p, C.c_void_p, C.c_int32, C.c_float, C.c_int32, C.c_void_p, C.c_void_p]
     lib.grpo_surrogate.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
                                    C.c_int32, C.c_void_p, C.c_double, C.c_double, C.c_int32, C.c_void_p, C.c_void_p]
+    lib.rg_phase_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_double)]
+    lib.rg_decode_attention_chunks.argtypes = [C.c_int32, C.c_int32, C.c_int32]
+    lib.rg_decode_attention_chunks.restype = C.c_int32
     lib.sagc_init.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state)]
     lib.sagc_group_stats.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p,
                                      C.c_void_p]
@@ -145,6 +158,34 @@ def _stream_ptr(stream=None) -> int:
 
 def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
+
+
+def _dev(name: str, t, dtype, shape=None, ndim=None):
+    """Checks that ``t`` is a contiguous tensor of ``dtype`` (a torch dtype or
+    a tuple of them) with ``shape`` (or ``ndim`` dimensions), in that order,
+    so that no kernel reads or writes past a buffer the caller sized
+    differently.  Raises TypeError / ValueError; returns ``t``.  Where it sits
+    (GPU memory) is checked by _gpu once every argument has passed this."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    dts = dtype if isinstance(dtype, tuple) else (dtype,)
+    if t.dtype not in dts:
+        raise TypeError(f"{name} must have dtype {' or '.join(str(d) for d in dts)}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimension(s), got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _gpu(**tensors):
+    """Every named tensor (None skipped) must be in GPU memory."""
+    for name, t in tensors.items():
+        if t is not None and t.device.type != "cuda":
+            raise TypeError(f"{name} must be in GPU memory, got device {t.device}")
 
 
 class Policy:
@@ -213,15 +254,16 @@ class Policy:
         packed, plen = _pack_prompts(prompts)
         P = len(plen)
         G = [int(g) for g in G]
+        if len(G) != P:
+            raise ValueError(f"G must have one entry per prompt ({P}), got {len(G)}")
         N = sum(G)
+        max_new = int(max_new)
         dev = packed.device
-        if out is None:
-            tokens = torch.empty((N, max_new), dtype=torch.int32, device=dev)
-            lengths = torch.empty(N, dtype=torch.int32, device=dev)
-            logprobs = torch.empty((N, max_new), dtype=torch.float32, device=dev)
-        else:
+        if out is not None:
             tokens, lengths, logprobs = out
-        dump = torch.empty((dump_steps, N, self.shape.vocab), dtype=torch.float32, device=dev) if dump_steps else None
+            _dev("tokens (out)", tokens, torch.int32, (N, max_new))
+            _dev("lengths (out)", lengths, torch.int32, (N,))
+            _dev("logprobs (out)", logprobs, torch.float32, (N, max_new))
         flags = ((0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
                  | (RG_FLAG_GROUP_PREFIX if group_prefix_pass else 0))
         kinds = 0
@@ -230,11 +272,26 @@ class Policy:
                 kinds |= 1 << KERNEL_KINDS.index(name)
         fl = None
         if forced_len is not None:
-            fl_np = np.ascontiguousarray(np.asarray(forced_len, dtype=np.int32))
+            if hasattr(forced_len, "detach"):
+                forced_len = forced_len.detach().cpu().numpy()
+            fl_np = np.ascontiguousarray(np.asarray(forced_len).reshape(-1))
+            if fl_np.shape != (N,):
+                raise ValueError(f"forced_len must have N = {N} entries, got {fl_np.size}")
+            if not np.issubdtype(fl_np.dtype, np.integer):
+                raise TypeError(f"forced_len must hold integers, got {fl_np.dtype}")
+            fl_np = fl_np.astype(np.int32)
             fl = fl_np.ctypes.data_as(C.POINTER(C.c_int32))
         ft = None
         if force_tokens is not None:
-            ft = force_tokens.to(device=dev, dtype=torch.int32).contiguous()
+            ft = _dev("force_tokens", force_tokens, torch.int32, (N, max_new))
+        _gpu(prompts=packed, force_tokens=ft)
+        if out is None:
+            tokens = torch.empty((N, max_new), dtype=torch.int32, device=dev)
+            lengths = torch.empty(N, dtype=torch.int32, device=dev)
+            logprobs = torch.empty((N, max_new), dtype=torch.float32, device=dev)
+        else:
+            _gpu(tokens=tokens, lengths=lengths, logprobs=logprobs)
+        dump = torch.empty((dump_steps, N, self.shape.vocab), dtype=torch.float32, device=dev) if dump_steps else None
         opts = rg_sampling(float(temperature), flags, fl, _ptr(ft), _ptr(dump), dump_steps, kinds)
         plen_a = (C.c_int32 * P)(*plen)
         g_a = (C.c_int32 * P)(*G)
@@ -256,11 +313,17 @@ class Policy:
         packed, plen = _pack_prompts(prompts)
         P = len(plen)
         G = [int(g) for g in G]
-        N, max_new = int(tokens.shape[0]), int(tokens.shape[1])
-        if N != sum(G):
-            raise ValueError("tokens must have sum(G) rows")
-        tokens = tokens.to(dtype=torch.int32).contiguous()
-        lengths = lengths.to(dtype=torch.int32).contiguous()
+        if len(G) != P:
+            raise ValueError(f"G must have one entry per prompt ({P}), got {len(G)}")
+        N = sum(G)
+        _dev("tokens", tokens, torch.int32, ndim=2)
+        if tokens.shape[0] != N:
+            raise ValueError(f"tokens must have sum(G) = {N} rows, got {tokens.shape[0]}")
+        max_new = int(tokens.shape[1])
+        _dev("lengths", lengths, torch.int32, (N,))
+        if out is not None:
+            _dev("logprobs (out)", out, torch.float32, (N, max_new))
+        _gpu(prompts=packed, tokens=tokens, lengths=lengths, out=out)
         lp = torch.empty((N, max_new), dtype=torch.float32, device=packed.device) if out is None else out
         flags = ((0 if share_prefix else RG_FLAG_NO_PREFIX_SHARING) | (RG_FLAG_PROFILE if profile else 0)
                  | (0 if row_tiles else RG_FLAG_NO_ROW_TILES))
@@ -278,6 +341,12 @@ class Policy:
         k = min(cap, n.value)
         return a[:k].copy(), g[:k].copy(), c[:k].copy()
 
+    def phase_times(self):
+        """(prefill_ms, decode_ms) of the last rollout on the device timeline."""
+        a, b = C.c_double(), C.c_double()
+        _check(load_library().rg_phase_times(self._h, C.byref(a), C.byref(b)))
+        return a.value, b.value
+
     def kernel_times(self, phase: int = 1) -> dict:
         lib = load_library()
         out = {}
@@ -292,6 +361,11 @@ def group_advantage(rewards, G_dev, eps: float = 1e-6, ddof: int = 1, out=None, 
     """rewards: device fp32 [N]; G_dev: device int32 [P]."""
     import torch
     lib = load_library()
+    _dev("rewards", rewards, torch.float32, ndim=1)
+    _dev("G", G_dev, torch.int32, ndim=1)
+    if out is not None:
+        _dev("adv (out)", out, torch.float32, tuple(rewards.shape))
+    _gpu(rewards=rewards, G=G_dev, out=out)
     if out is None:
         out = torch.empty_like(rewards)
     _check(lib.group_advantage(_ptr(rewards), _ptr(G_dev), int(G_dev.numel()), int(rewards.numel()), float(eps),
@@ -308,7 +382,17 @@ def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps
     fraction, counted tokens, counted sequences)."""
     import torch
     lib = load_library()
+    _dev("new_lp", new_lp, torch.float32, ndim=2)
     N, max_new = int(new_lp.shape[0]), int(new_lp.shape[1])
+    _dev("old_lp", old_lp, torch.float32, (N, max_new))
+    _dev("adv", adv, torch.float32, (N,))
+    _dev("lengths", lengths, torch.int32, (N,))
+    _dev("G", G_dev, torch.int32, ndim=1)
+    if keep is not None:
+        _dev("keep", keep, torch.int32, tuple(G_dev.shape))
+    if mode not in LOSS_MODES:
+        raise ValueError(f"mode must be one of {sorted(LOSS_MODES)}")
+    _gpu(new_lp=new_lp, old_lp=old_lp, adv=adv, lengths=lengths, G=G_dev, keep=keep)
     out = torch.empty(4, dtype=torch.float64, device=new_lp.device)
     _check(lib.grpo_surrogate(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()),
                               N, max_new, _ptr(keep), float(eps_lo), float(eps_hi), LOSS_MODES[mode], _ptr(out),
@@ -321,6 +405,9 @@ def group_filter(rewards, G_dev, stream=None):
     tensors (keep [P], kept_ids [P], n_kept [1]) as written by the library."""
     import torch
     lib = load_library()
+    _dev("rewards", rewards, torch.float32, ndim=1)
+    _dev("G", G_dev, torch.int32, ndim=1)
+    _gpu(rewards=rewards, G=G_dev)
     P = int(G_dev.numel())
     keep = torch.empty(P, dtype=torch.int32, device=rewards.device)
     kept = torch.full((P,), -1, dtype=torch.int32, device=rewards.device)
@@ -334,7 +421,10 @@ def philox_blocks(key0: int, key1: int, ctr, stream=None):
     """ctr: device int64/uint64 tensor [n, 4] (bit patterns); returns [n, 4]."""
     import torch
     lib = load_library()
-    ctr = ctr.contiguous()
+    _dev("ctr", ctr, (torch.int64, torch.uint64), ndim=2)
+    if ctr.shape[1] != 4:
+        raise ValueError(f"ctr must have shape [n, 4], got {tuple(ctr.shape)}")
+    _gpu(ctr=ctr)
     out = torch.empty_like(ctr)
     _check(lib.rg_philox_blocks(C.c_uint64(key0), C.c_uint64(key1), _ptr(ctr), ctr.shape[0], _ptr(out),
                                 _stream_ptr(stream)))
@@ -376,9 +466,14 @@ class Sagc:
         float [P, 4] = (l_max, l_median, R, S)."""
         import torch
         lib = load_library()
+        _dev("lengths", lengths, torch.int32, ndim=1)
+        _dev("G", G_dev, torch.int32, ndim=1)
         P = int(G_dev.numel())
         if out is None:
             out = torch.empty((P, 4), dtype=torch.float32, device=lengths.device)
+        else:
+            _dev("stats (out)", out, torch.float32, (P, 4))
+        _gpu(lengths=lengths, G=G_dev, out=out)
         _check(lib.sagc_group_stats(_ptr(lengths), _ptr(G_dev), P, int(lengths.numel()), self.cfg.tau, _ptr(out),
                                     _stream_ptr(stream)))
         return out
@@ -401,6 +496,13 @@ class Sagc:
         return {"lambda": st.lam, "alpha": list(st.alpha[:k]), "beta": list(st.beta[:k]), "g_index": st.g_index,
                 "step": st.step, "last_rate": st.last_rate, "last_sample": list(st.last_sample[:k]),
                 "last_score": list(st.last_score[:k])}
+
+
+def decode_attention_chunks(rows: int, n_kv: int, ctx_max: int) -> int:
+    """Context chunks per row of a decode step's attention (see rollout.h)."""
+    n = load_library().rg_decode_attention_chunks(int(rows), int(n_kv), int(ctx_max))
+    _check(min(n, 0))
+    return n
 
 
 def sagc_beta_draw(seed: int, step: int, arm: int, a: float, b: float) -> float:

@@ -18,6 +18,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -117,6 +118,8 @@ struct rg_policy {
   int64_t kt_n[2][RG_K_COUNT]{};
 
   int32_t last_steps = 0;
+  hipEvent_t phase_ev[3]{};   // start of prefill, end of prefill + fork, end of decode (last rollout_group)
+  bool phase_valid = false;
 
   hipStream_t cap_st = nullptr;   // private stream used only to capture decode-step graphs
   bool use_graphs = true;
@@ -137,6 +140,7 @@ struct rg_policy {
     if (h_ring) (void)hipHostFree(h_ring);
     for (auto& e : ring_ev) if (e) (void)hipEventDestroy(e);
     for (auto& e : prof_ev) if (e) (void)hipEventDestroy(e);
+    for (auto& e : phase_ev) if (e) (void)hipEventDestroy(e);
     if (cap_st) (void)hipStreamDestroy(cap_st);
   }
 };
@@ -598,8 +602,11 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       lim.kv_pool_pages < 0)
     return fail(RG_EINVAL, "rg_policy_create: invalid limits");
 
-  rg_policy* pol = new rg_policy();
-  auto bail = [&](int rc) { delete pol; return rc; };
+  // Owned here until creation succeeds: every early return (HIPTRY included)
+  // frees the policy and the device memory it holds so far.
+  std::unique_ptr<rg_policy> owner(new rg_policy());
+  rg_policy* pol = owner.get();
+  auto bail = [](int rc) { return rc; };
   pol->cfg = c;
   pol->lim = lim;
   pol->dtype = c.dtype;
@@ -782,6 +789,10 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
       e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
       if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipEventCreate: ") + hipGetErrorString(e)));
     }
+    for (auto& ev : pol->phase_ev) {
+      e = hipEventCreate(&ev);
+      if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipEventCreate: ") + hipGetErrorString(e)));
+    }
     e = hipStreamCreateWithFlags(&pol->cap_st, hipStreamNonBlocking);
     if (e != hipSuccess) return bail(fail(RG_EHIP, std::string("hipStreamCreate: ") + hipGetErrorString(e)));
     const char* env = getenv("RG_NO_GRAPHS");
@@ -789,7 +800,7 @@ int rg_policy_create(const rg_config* cfg, const rg_weights* w, const rg_limits*
     const char* pe = getenv("RG_PROGRESS");
     pol->progress_every = pe ? std::max(0, atoi(pe)) : 0;
   }
-  *out = pol;
+  *out = owner.release();
   return RG_OK;
 }
 
@@ -821,9 +832,12 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
   if ((rc = prof_begin(pol, (o.flags & RG_FLAG_PROFILE) != 0, o.profile_kinds))) return rc;
   if ((rc = stage_groups(pol, st, gr, prompt_len, G, o.forced_len))) return rc;
   const int32_t* forced_dev = o.forced_len ? pol->seq_forced : nullptr;
+  pol->phase_valid = false;
+  HIPTRY(hipEventRecord(pol->phase_ev[0], st));
   if ((rc = prefill_and_fork(pol, st, gr, prompts, prompt_len, G, max_new, !(o.flags & RG_FLAG_NO_PREFIX_SHARING),
                              tokens, logprobs)))
     return rc;
+  HIPTRY(hipEventRecord(pol->phase_ev[1], st));
 
   // ---- sampling / retirement of one step
   SampleArgs sm{};
@@ -910,7 +924,9 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
       fflush(stderr);
     }
   }
+  HIPTRY(hipEventRecord(pol->phase_ev[2], st));
   HIPTRY(hipStreamSynchronize(st));
+  pol->phase_valid = true;
   // snapshots the loop has not read yet (at most RG_LOOKAHEAD of them)
   for (int k = known_t + 1; k <= last_t; ++k) {
     const int nx = k % RG_RING;
@@ -1074,6 +1090,22 @@ int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t
   if (groups) HIPTRY(hipMemcpy(groups, pol->hist_groups, (size_t)n * 4, hipMemcpyDeviceToHost));
   if (ctx) HIPTRY(hipMemcpy(ctx, pol->hist_ctx, (size_t)n * 8, hipMemcpyDeviceToHost));
   return RG_OK;
+}
+
+int rg_phase_times(const rg_policy* pol, double* prefill_ms, double* decode_ms) {
+  if (!pol) return fail(RG_EINVAL, "rg_phase_times: NULL policy");
+  if (!pol->phase_valid) return fail(RG_EINVAL, "rg_phase_times: no completed rollout_group call");
+  float a = 0.f, b = 0.f;
+  HIPTRY(hipEventElapsedTime(&a, pol->phase_ev[0], pol->phase_ev[1]));
+  HIPTRY(hipEventElapsedTime(&b, pol->phase_ev[1], pol->phase_ev[2]));
+  if (prefill_ms) *prefill_ms = a;
+  if (decode_ms) *decode_ms = b;
+  return RG_OK;
+}
+
+int32_t rg_decode_attention_chunks(int32_t rows, int32_t n_kv, int32_t ctx_max) {
+  if (rows < 1 || n_kv < 1 || ctx_max < 1) return fail(RG_EINVAL, "rg_decode_attention_chunks: bad argument");
+  return att_row_chunks(row_bucket(rows), n_kv, ctx_max);
 }
 
 int rg_kernel_times(const rg_policy* pol, int32_t phase, int32_t kind, double* total_ms, int64_t* launches) {

@@ -75,8 +75,10 @@ ADVANTAGE_SLIPS = {
 
 
 SAGC_PINS = [sagc_pins.test_group_stats_worked_examples, sagc_pins.test_group_stats_match_numpy,
-             sagc_pins.test_dual_and_posterior_worked_example, sagc_pins.test_choice_rules] + \
-    [lambda s=s: sagc_pins.test_closed_loop_separates_arms(s) for s in (0, 1)]
+             sagc_pins.test_dual_and_posterior_worked_example, sagc_pins.test_choice_rules,
+             sagc_pins.test_initial_size_state] + \
+    [lambda s=s: sagc_pins.test_closed_loop_separates_arms(s) for s in (0, 1)] + \
+    [lambda z=z: sagc_pins.test_initial_size_is_uniform_over_the_admitted_sizes(z) for z in ((4, 8, 16), (2, 4))]
 
 SAGC_SLIPS = {
     "stats_even_median_upper": ("group_stats", "(seg[g // 2 - 1] + seg[g // 2]) / 2.0", "float(seg[g // 2])"),
@@ -92,6 +94,9 @@ SAGC_SLIPS = {
     "choice_ties_to_larger": ("sagc_choose", "scores[i] > scores[best]", "scores[i] >= scores[best]"),
     "choice_penalty_sign": ("sagc_choose", "- lam * samples[i]", "+ lam * samples[i]"),
     "choice_whole_range": ("sagc_choose", "(g_index - 1, g_index, g_index + 1)", "range(k)"),
+    "init_never_largest": ("sagc_init", "int(u53(w[0]) * k)", "int(u53(w[0]) * (k - 1))"),
+    "init_rounded": ("sagc_init", "int(u53(w[0]) * k)", "int(round(u53(w[0]) * (k - 1)))"),
+    "init_low_half_only": ("sagc_init", "int(u53(w[0]) * k)", "int(u53(w[0] & 0xFFFFFFFF) * k)"),
 }
 
 

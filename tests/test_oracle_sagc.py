@@ -127,3 +127,22 @@ def test_closed_loop_separates_arms(seed):
     assert risk[29][2] > risk[29][1] > risk[29][0]     # p16 > p8 > p4 by step 30
     assert risk[-1][2] > risk[-1][1] > risk[-1][0]
     assert st.lam >= 0.0
+
+
+@pytest.mark.parametrize("sizes", [(4, 8, 16), (2, 4), (4, 8, 16, 32, 64)])
+def test_initial_size_is_uniform_over_the_admitted_sizes(sizes):
+    """Algorithm 1 starts from a size drawn at random from the admitted list:
+    over 3,000 seeds every size is drawn, and the counts pass a chi-square
+    test against the uniform distribution."""
+    n = 3000
+    idx = [O.sagc_init(O.SagcConfig(sizes=sizes, seed=s)).g_index for s in range(n)]
+    assert min(idx) >= 0 and max(idx) < len(sizes)
+    counts = np.bincount(idx, minlength=len(sizes))
+    assert np.all(counts > 0), counts
+    assert ss.chisquare(counts).pvalue > 1e-3, counts
+
+
+def test_initial_size_state():
+    st = O.sagc_init(O.SagcConfig(sizes=(4, 8, 16), seed=3))
+    assert st.lam == 0.0 and st.step == 0
+    assert st.alpha == [1.0] * 3 and st.beta == [1.0] * 3
