@@ -370,7 +370,7 @@ def ceilings():
         ms = best_ms(lambda: torch.matmul(x, wt))
         fl = 2.0 * m * nn * k
         g[name] = {"m_n_k": [m, nn, k], "ms": round(ms, 4), "TFLOPs": round(fl / ms / 1e9, 1),
-                   "frac_of_spec": round(fl / ms / 1e3 / MFMA_BF16_PEAK, 4)}
+                   "frac_of_spec": round(fl / (ms / 1e3) / MFMA_BF16_PEAK, 4)}
         del x, w, wt
     res["bf16_gemm_torch_matmul"] = g
     print(json.dumps(res), flush=True)
@@ -451,7 +451,7 @@ def main():
                     group_prefix_pass=args.group_prefix, out=(tokens, lengths, logprobs))
         rg.group_advantage(rewards, G_dev, 1e-6, 1, out=adv)
 
-    breakdown, dom = {}, None
+    breakdown, dom, prefill_kt, by_bucket = {}, None, {}, {}
     for i in range(args.warmup):
         # the first warmup step times every kernel class (untimed step): the
         # per-class breakdown, and the dominant class timed in the timed steps
@@ -459,6 +459,13 @@ def main():
         if profile and i == 0:
             breakdown = pol.kernel_times(1)
             dom = max(breakdown.items(), key=lambda kv: kv[1][0])[0]
+            prefill_kt = pol.kernel_times(0)
+            by_bucket = {}
+            for b, name in enumerate(("16", "32", "64", "128", "256", "384", "512", "more")):
+                kb = {k: round(v[0], 2) for k, v in pol.kernel_times(2 + b).items() if v[1]}
+                if kb:
+                    steps = pol.kernel_times(2 + b)["compact"][1]
+                    by_bucket[name] = {"steps": steps, "ms": kb}
         print(f"# warmup step {i} done", file=sys.stderr, flush=True)
     if profile and dom is None:
         dom = "attn"
@@ -521,6 +528,9 @@ def main():
         dec_ms = sum(v[0] for v in breakdown.values())
         tot_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
         res["decode_hbm_frac_kernel_time"] = round(tot_b / (dec_ms / 1e3) / HBM_PEAK, 4)
+        res["kernel_ms_by_row_bucket_untimed_step"] = by_bucket
+        res["prefill_kernel_ms_untimed_step"] = {k: round(v[0], 2) for k, v in
+                                                 sorted(prefill_kt.items(), key=lambda kv: -kv[1][0]) if v[1]}
     if profile and kt:
         alg, _ = algorithmic_bytes(shape, hist_a, hist_g, hist_c, wl.prompt_len)
         name, (ms_tot, n_tot) = next(iter(kt.items()))

@@ -334,9 +334,12 @@ int32_t rg_decode_attention_chunks(int32_t rows, int32_t n_kv, int32_t ctx_max);
 #define RG_K_SETUP     14
 #define RG_K_LOGPROB   15   /* token log-probability gather of recompute_logprobs */
 #define RG_K_COUNT     16
-/* Totals for kernel class `kind` over the decode steps (phase 1) or the
- * prefill (phase 0) of the last profiled rollout: summed launch durations in
- * milliseconds (HIP events) and the number of launches. */
+/* Totals for kernel class `kind` over the prefill (phase 0), every decode
+ * step (phase 1) or the decode steps of one row bucket (phase 2 + b for the
+ * buckets of at most 16, 32, 64, 128, 256, 384, 512 rows and b = 7 for
+ * larger ones) of the last profiled rollout: summed launch durations in
+ * milliseconds (HIP events) and the number of launches.  recompute_logprobs
+ * records its prompt prefill as phase 0 and its completion rows as phase 1. */
 int rg_kernel_times(const rg_policy* pol, int32_t phase, int32_t kind, double* total_ms,
                     int64_t* launches);
 

@@ -52,6 +52,7 @@ constexpr int RG_LOOKAHEAD = 4;        // decode steps enqueued beyond the last 
 constexpr int RG_PROF_RING = 8192;     // event pairs in flight when profiling
 constexpr int RG_SAMPLE_SLICES_MAX = 32;  // vocabulary slices per sampled row
 constexpr int RG_LM_SLICE_ROWS = 2048;    // recompute: lm-head rows per slice (when the activations hold them)
+constexpr int RG_PROF_PHASES = 2 + 8;     // prefill, decode, decode by row bucket (16 .. 512, larger)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -114,8 +115,9 @@ struct rg_policy {
   std::vector<hipEvent_t> prof_ev;  // 2 * RG_PROF_RING
   std::vector<int> prof_kind, prof_ph;
   int64_t prof_head = 0, prof_tail = 0;
-  double kt_ms[2][RG_K_COUNT]{};
-  int64_t kt_n[2][RG_K_COUNT]{};
+  // [0] prefill, [1] decode (all steps), [2 + b] decode steps of row bucket b
+  double kt_ms[RG_PROF_PHASES][RG_K_COUNT]{};
+  int64_t kt_n[RG_PROF_PHASES][RG_K_COUNT]{};
 
   int32_t last_steps = 0;
   hipEvent_t phase_ev[3]{};   // start of prefill, end of prefill + fork, end of decode (last rollout_group)
@@ -170,8 +172,13 @@ int prof_drain_one(rg_policy* p) {
   HIPTRY(hipEventSynchronize(p->prof_ev[2 * i + 1]));
   float ms = 0.f;
   HIPTRY(hipEventElapsedTime(&ms, p->prof_ev[2 * i], p->prof_ev[2 * i + 1]));
-  p->kt_ms[p->prof_ph[i]][p->prof_kind[i]] += ms;
-  p->kt_n[p->prof_ph[i]][p->prof_kind[i]] += 1;
+  const int ph = p->prof_ph[i], k = p->prof_kind[i];
+  p->kt_ms[ph][k] += ms;
+  p->kt_n[ph][k] += 1;
+  if (ph >= 2) {   // a decode step of one row bucket also counts towards the decode total
+    p->kt_ms[1][k] += ms;
+    p->kt_n[1][k] += 1;
+  }
   p->prof_tail++;
   return RG_OK;
 }
@@ -393,6 +400,15 @@ int row_bucket(int m) {
   if (m <= 256) return 256;
   if (m <= 384) return 384;
   return (int)ceil_div(m, 256) * 256;
+}
+
+// Profiling phase of a decode step with row bound rows_ub: 2 + the index of
+// its row bucket (16, 32, 64, 128, 256, 384, 512, larger).
+int bucket_phase(int rows_ub) {
+  const int edges[7] = {16, 32, 64, 128, 256, 384, 512};
+  int b = 0;
+  while (b < 7 && rows_ub > edges[b]) ++b;
+  return 2 + b;
 }
 
 // Vocabulary slices per sampled row: about 1024 blocks in all.
@@ -915,6 +931,7 @@ int rollout_group(rg_policy* pol, const int32_t* prompts, const int32_t* prompt_
       graphs.launched_on = st;
       HIPTRY(hipGraphLaunch(exec, st));
     } else {
+      pol->prof_phase = bucket_phase(rows_ub);
       if ((rc = enqueue_step(pol, st, rows_ub, ctx_all, sm, ca, pre))) return rc;
     }
     if ((rc = snapshot(t))) return rc;
@@ -1109,7 +1126,8 @@ int32_t rg_decode_attention_chunks(int32_t rows, int32_t n_kv, int32_t ctx_max) 
 }
 
 int rg_kernel_times(const rg_policy* pol, int32_t phase, int32_t kind, double* total_ms, int64_t* launches) {
-  if (!pol || phase < 0 || phase > 1 || kind < 0 || kind >= RG_K_COUNT) return fail(RG_EINVAL, "rg_kernel_times: bad argument");
+  if (!pol || phase < 0 || phase >= RG_PROF_PHASES || kind < 0 || kind >= RG_K_COUNT)
+    return fail(RG_EINVAL, "rg_kernel_times: bad argument");
   if (total_ms) *total_ms = pol->kt_ms[phase][kind];
   if (launches) *launches = pol->kt_n[phase][kind];
   return RG_OK;
