@@ -268,13 +268,19 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
  *                   counted tokens and the counted sequences.  All zero when
  *                   nothing is counted; NaN in all four if G is invalid or a
  *                   length lies outside [1, max_new].
- * One workgroup; the summation order is fixed, so results are reproducible.
- * Only enqueues work on `stream`; allocates nothing.  Errors: RG_EINVAL for
- * NULL pointers, P, N or max_new < 1, eps_lo outside [0, 1), eps_hi < 0 or an
- * unknown mode. */
+ * Two kernels: one wave per sequence sums its terms (fp64) into a 16-byte
+ * record of device scratch, then one workgroup adds the records group by
+ * group in sequence order; the summation order is fixed, so results are
+ * reproducible.  The scratch (16*N bytes) is taken with hipMallocAsync on
+ * `stream` and released with hipFreeAsync after the kernels, so concurrent
+ * calls on different streams do not share it.  Only enqueues work on
+ * `stream`.  Errors: RG_EINVAL for NULL pointers, P, N or max_new < 1, eps_lo
+ * outside [0, 1), eps_hi < 0 or an unknown mode; RG_EHIP when the scratch
+ * cannot be allocated. */
 int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
                    const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep,
                    double eps_lo, double eps_hi, int32_t mode, double* out, void* stream);
+
 
 /* ---- test and measurement hooks ---- */
 

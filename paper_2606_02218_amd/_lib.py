@@ -377,9 +377,10 @@ LOSS_MODES = {"token": 0, "seq": 1}
 
 
 def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps_hi: float = 0.2,
-                   mode: str = "token", keep=None, stream=None):
+                   mode: str = "token", keep=None, stream=None, out=None):
     """Clipped surrogate; returns a device fp64 tensor (loss, clipped
-    fraction, counted tokens, counted sequences)."""
+    fraction, counted tokens, counted sequences), written into ``out`` when
+    given."""
     import torch
     lib = load_library()
     _dev("new_lp", new_lp, torch.float32, ndim=2)
@@ -392,11 +393,13 @@ def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps
         _dev("keep", keep, torch.int32, tuple(G_dev.shape))
     if mode not in LOSS_MODES:
         raise ValueError(f"mode must be one of {sorted(LOSS_MODES)}")
-    _gpu(new_lp=new_lp, old_lp=old_lp, adv=adv, lengths=lengths, G=G_dev, keep=keep)
-    out = torch.empty(4, dtype=torch.float64, device=new_lp.device)
-    _check(lib.grpo_surrogate(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()),
-                              N, max_new, _ptr(keep), float(eps_lo), float(eps_hi), LOSS_MODES[mode], _ptr(out),
-                              _stream_ptr(stream)))
+    if out is not None:
+        _dev("out", out, torch.float64, (4,))
+    _gpu(new_lp=new_lp, old_lp=old_lp, adv=adv, lengths=lengths, G=G_dev, keep=keep, out=out)
+    if out is None:
+        out = torch.empty(4, dtype=torch.float64, device=new_lp.device)
+    _check(lib.grpo_surrogate(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()), N, max_new,
+              _ptr(keep), float(eps_lo), float(eps_hi), LOSS_MODES[mode], _ptr(out), _stream_ptr(stream)))
     return out
 
 

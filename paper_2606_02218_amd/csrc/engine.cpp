@@ -1046,19 +1046,40 @@ int recompute_logprobs(rg_policy* pol, const int32_t* prompts, const int32_t* pr
   return RG_OK;
 }
 
+namespace {
+// Arguments of the clipped surrogate, checked on the host.
+int surrogate_args(const char* who, const float* new_lp, const float* old_lp, const float* adv,
+                   const int32_t* lengths, const int32_t* G, int32_t P, int32_t N, int32_t max_new,
+                   const int32_t* keep, double eps_lo, double eps_hi, int32_t mode, double* out, SurrogateArgs* sa) {
+  const std::string w(who);
+  if (!new_lp || !old_lp || !adv || !lengths || !G || !out) return fail(RG_EINVAL, w + ": NULL argument");
+  if (P < 1 || N < 1 || max_new < 1) return fail(RG_EINVAL, w + ": P, N and max_new must be >= 1");
+  if (!(eps_lo >= 0.0 && eps_lo < 1.0) || !(eps_hi >= 0.0) || !std::isfinite(eps_hi))
+    return fail(RG_EINVAL, w + ": need 0 <= eps_lo < 1 and 0 <= eps_hi");
+  if (mode != RG_LOSS_TOKEN_MEAN && mode != RG_LOSS_SEQ_MEAN) return fail(RG_EINVAL, w + ": unknown mode");
+  *sa = SurrogateArgs{};
+  sa->new_lp = new_lp; sa->old_lp = old_lp; sa->adv = adv; sa->lengths = lengths; sa->G = G; sa->keep = keep;
+  sa->P = P; sa->N = N; sa->max_new = max_new; sa->mode = mode; sa->eps_lo = eps_lo; sa->eps_hi = eps_hi;
+  sa->out = out;
+  return RG_OK;
+}
+}  // namespace
+
 int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
                    const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep, double eps_lo,
                    double eps_hi, int32_t mode, double* out, void* stream) {
-  if (!new_lp || !old_lp || !adv || !lengths || !G || !out) return fail(RG_EINVAL, "grpo_surrogate: NULL argument");
-  if (P < 1 || N < 1 || max_new < 1) return fail(RG_EINVAL, "grpo_surrogate: P, N and max_new must be >= 1");
-  if (!(eps_lo >= 0.0 && eps_lo < 1.0) || !(eps_hi >= 0.0) || !std::isfinite(eps_hi))
-    return fail(RG_EINVAL, "grpo_surrogate: need 0 <= eps_lo < 1 and 0 <= eps_hi");
-  if (mode != RG_LOSS_TOKEN_MEAN && mode != RG_LOSS_SEQ_MEAN) return fail(RG_EINVAL, "grpo_surrogate: unknown mode");
-  SurrogateArgs sa{};
-  sa.new_lp = new_lp; sa.old_lp = old_lp; sa.adv = adv; sa.lengths = lengths; sa.G = G; sa.keep = keep;
-  sa.P = P; sa.N = N; sa.max_new = max_new; sa.mode = mode; sa.eps_lo = eps_lo; sa.eps_hi = eps_hi; sa.out = out;
-  const hipError_t e = launch_surrogate(sa, (hipStream_t)stream);
+  SurrogateArgs sa;
+  int rc = surrogate_args("grpo_surrogate", new_lp, old_lp, adv, lengths, G, P, N, max_new, keep, eps_lo, eps_hi,
+                          mode, out, &sa);
+  if (rc) return rc;
+  // per-sequence records: stream-ordered scratch of this call alone
+  hipStream_t st = (hipStream_t)stream;
+  SurrogateRec* rec = nullptr;
+  HIPTRY(hipMallocAsync((void**)&rec, (size_t)N * sizeof(SurrogateRec), st));
+  const hipError_t e = launch_surrogate(sa, rec, st);
+  const hipError_t ef = hipFreeAsync(rec, st);
   if (e != hipSuccess) return fail(RG_EHIP, std::string("grpo_surrogate launch: ") + hipGetErrorString(e));
+  if (ef != hipSuccess) return fail(RG_EHIP, std::string("grpo_surrogate hipFreeAsync: ") + hipGetErrorString(ef));
   return RG_OK;
 }
 

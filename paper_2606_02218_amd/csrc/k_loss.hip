@@ -182,16 +182,45 @@ __global__ __launch_bounds__(LP_THREADS) void k_token_logprob(const float* __res
   if (tid == 0) lp[out[r]] = z[tgt[r]] / T - (sm[0] + logf(ss[0]));
 }
 
-// Clipped surrogate.  One block of 1024 threads: tiles of 1024 groups get
-// their sequence offsets from the block scan, then each wave takes whole
-// groups; its lanes stride over a member's tokens and accumulate
-// min(rho * A, clip(rho, 1 - eps_lo, 1 + eps_hi) * A), rho = exp(new - old),
-// in fp64.  Per-wave totals are combined in wave order, so the result does
-// not depend on timing.  out = (loss, clipped fraction, tokens, sequences);
-// NaN in all four for invalid G or a length outside [1, max_new].
-__global__ __launch_bounds__(1024) void k_surrogate(SurrogateArgs a) {
+// Clipped surrogate, pass 1: one wave per sequence s < N.  Its lanes stride
+// over the sequence's L_s tokens and accumulate, in fp64,
+// min(rho * A_s, clip(rho, 1 - eps_lo, 1 + eps_hi) * A_s), rho = exp(new - old),
+// then the wave sums them (a butterfly: a fixed order).  rec[s] = (sum,
+// clipped tokens); a length outside [1, max_new] writes clipped = -1.
+__global__ __launch_bounds__(256) void k_surrogate_seq(SurrogateArgs a, SurrogateRec* __restrict__ rec) {
+  const int lane = threadIdx.x & 63;
+  const int s = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (s >= a.N) return;
+  const int L = a.lengths[s];
+  if (L < 1 || L > a.max_new) {
+    if (lane == 0) rec[s] = SurrogateRec{0.0, -1, 0};
+    return;
+  }
+  const double A = (double)a.adv[s];
+  const int64_t row = (int64_t)s * a.max_new;
+  double acc = 0.0;
+  int clips = 0;
+  for (int i = lane; i < L; i += 64) {
+    const double rho = exp((double)a.new_lp[row + i] - (double)a.old_lp[row + i]);
+    const double un = rho * A;
+    const double cl = fmin(fmax(rho, 1.0 - a.eps_lo), 1.0 + a.eps_hi) * A;
+    acc += fmin(un, cl);
+    clips += cl < un;
+  }
+  acc = wave_sum_d(acc);
+  for (int o = 32; o > 0; o >>= 1) clips += __shfl_xor(clips, o, 64);
+  if (lane == 0) rec[s] = SurrogateRec{acc, clips, 0};
+}
+
+// Pass 2, one block of 1024 threads: the group partition (each G[p] >= 1,
+// sum N), then thread t takes groups t, t + 1024, ... whose keep flag is set
+// and adds their members' records in sequence order; the per-thread totals
+// are combined by a butterfly within each wave and the wave totals in wave
+// order, so the result does not depend on timing.  out = (loss, clipped
+// fraction, tokens, sequences); NaN in all four for an invalid partition or
+// a length outside [1, max_new], zeros when nothing is counted.
+__global__ __launch_bounds__(1024) void k_surrogate_reduce(SurrogateArgs a, const SurrogateRec* __restrict__ rec) {
   __shared__ int lds[17];
-  __shared__ int offs[1025];
   __shared__ double w_tok[16], w_seq[16];
   __shared__ long long w_ntok[16], w_nclip[16];
   __shared__ int w_nseq[16], w_bad[16];
@@ -209,40 +238,30 @@ __global__ __launch_bounds__(1024) void k_surrogate(SurrogateArgs a) {
     const int g = p < a.P ? a.G[p] : 0;
     int t;
     const int o = block_excl_scan(g, lds, &t) + carry;
-    offs[tid] = o;
-    if (tid == blockDim.x - 1) offs[blockDim.x] = o + g;
-    __syncthreads();
-    const int ng = min((int)blockDim.x, a.P - base);
-    for (int k = wave; k < ng; k += nw) {
-      if (a.keep && a.keep[base + k] == 0) continue;
-      for (int s = offs[k]; s < offs[k + 1]; ++s) {
-        const int L = a.lengths[s];
-        if (L < 1 || L > a.max_new) {
+    if (p < a.P && (!a.keep || a.keep[p] != 0)) {
+      for (int s = o; s < o + g; ++s) {
+        const SurrogateRec r = rec[s];
+        if (r.clips < 0) {
           bad = 1;
           continue;
         }
-        const double A = (double)a.adv[s];
-        const int64_t row = (int64_t)s * a.max_new;
-        double acc = 0.0;
-        int clips = 0;
-        for (int i = lane; i < L; i += 64) {
-          const double rho = exp((double)a.new_lp[row + i] - (double)a.old_lp[row + i]);
-          const double un = rho * A;
-          const double cl = fmin(fmax(rho, 1.0 - a.eps_lo), 1.0 + a.eps_hi) * A;
-          acc += fmin(un, cl);
-          clips += cl < un;
-        }
-        acc = wave_sum_d(acc);
-        for (int o2 = 32; o2 > 0; o2 >>= 1) clips += __shfl_xor(clips, o2, 64);
-        tok_sum += acc;
-        seq_sum += acc / (double)L;
+        const int L = a.lengths[s];
+        tok_sum += r.acc;
+        seq_sum += r.acc / (double)L;
         n_tok += L;
-        n_clip += clips;
+        n_clip += r.clips;
         n_seq += 1;
       }
     }
     carry += t;
-    __syncthreads();
+  }
+  tok_sum = wave_sum_d(tok_sum);
+  seq_sum = wave_sum_d(seq_sum);
+  for (int o = 32; o > 0; o >>= 1) {
+    n_tok += __shfl_xor(n_tok, o, 64);
+    n_clip += __shfl_xor(n_clip, o, 64);
+    n_seq += __shfl_xor(n_seq, o, 64);
+    bad |= __shfl_xor(bad, o, 64);
   }
   if (lane == 0) {
     w_tok[wave] = tok_sum; w_seq[wave] = seq_sum; w_ntok[wave] = n_tok; w_nclip[wave] = n_clip;
@@ -307,7 +326,9 @@ hipError_t launch_token_logprob(const float* logits, int V, float T, const int32
   return hipGetLastError();
 }
 
-hipError_t launch_surrogate(const SurrogateArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_surrogate, dim3(1), dim3(1024), 0, st, a);
+hipError_t launch_surrogate(const SurrogateArgs& a, SurrogateRec* rec, hipStream_t st) {
+  if (a.N < 1 || !rec) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_surrogate_seq, dim3((a.N + 3) / 4), dim3(256), 0, st, a, rec);
+  hipLaunchKernelGGL(k_surrogate_reduce, dim3(1), dim3(1024), 0, st, a, (const SurrogateRec*)rec);
   return hipGetLastError();
 }

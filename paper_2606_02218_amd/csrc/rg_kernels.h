@@ -282,4 +282,16 @@ struct SurrogateArgs {
   double eps_lo, eps_hi;
   double* out;
 };
-hipError_t launch_surrogate(const SurrogateArgs& a, hipStream_t st);
+// Per-sequence record of the clipped surrogate's first pass (16 bytes):
+// the fp64 sum of the sequence's terms and its clipped-token count (-1 for a
+// length outside [1, max_new]).
+struct SurrogateRec {
+  double acc;
+  int32_t clips;
+  int32_t pad;
+};
+static_assert(sizeof(SurrogateRec) == 16, "surrogate record layout");
+// Two launches: per-sequence records into rec [N] (device scratch), then one
+// block that reduces them in a fixed order into a.out.
+hipError_t launch_surrogate(const SurrogateArgs& a, SurrogateRec* rec, hipStream_t st);
+
