@@ -281,6 +281,21 @@ int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, c
                    const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep,
                    double eps_lo, double eps_hi, int32_t mode, double* out, void* stream);
 
+/* grpo_surrogate for callers that cannot allocate device memory: code under
+ * HIP graph capture, serving loops that must not call hipMalloc, harnesses
+ * that forbid allocation.  Same arguments, checks, kernels and result (bit
+ * for bit) as grpo_surrogate, but the per-sequence records go to a static
+ * device array of the library, so the call allocates nothing.
+ *   Limit: N <= 65536 (the array holds 65536 records of 16 bytes: 1 MiB on
+ *   every device the library runs on, held until the process ends); a larger
+ *   N gives RG_EINVAL before any device work.
+ * Every call on one device uses that device's array: calls that overlap on
+ * one device (other streams or threads) race and must be serialized by the
+ * caller.  Nothing in it needs clearing: a call writes every record it reads.
+ * Only enqueues work on `stream`. */
+int grpo_surrogate_noalloc(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
+                           const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep,
+                           double eps_lo, double eps_hi, int32_t mode, double* out, void* stream);
 
 /* ---- test and measurement hooks ---- */
 

@@ -21,7 +21,8 @@ KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge"
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
            "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
            "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter",
-           "recompute_logprobs", "grpo_surrogate", "rg_decode_attention_chunks", "rg_phase_times"]
+           "recompute_logprobs", "grpo_surrogate", "rg_decode_attention_chunks", "rg_phase_times",
+           "grpo_surrogate_noalloc"]
 SAGC_MAX_SIZES = 8
 
 
@@ -130,6 +131,7 @@ def load_library():
     lib.rg_phase_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_double)]
     lib.rg_decode_attention_chunks.argtypes = [C.c_int32, C.c_int32, C.c_int32]
     lib.rg_decode_attention_chunks.restype = C.c_int32
+    lib.grpo_surrogate_noalloc.argtypes = lib.grpo_surrogate.argtypes
     lib.sagc_init.argtypes = [C.POINTER(sagc_config), C.POINTER(sagc_state)]
     lib.sagc_group_stats.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p,
                                      C.c_void_p]
@@ -377,10 +379,11 @@ LOSS_MODES = {"token": 0, "seq": 1}
 
 
 def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps_hi: float = 0.2,
-                   mode: str = "token", keep=None, stream=None, out=None):
+                   mode: str = "token", keep=None, stream=None, out=None, noalloc: bool = False):
     """Clipped surrogate; returns a device fp64 tensor (loss, clipped
     fraction, counted tokens, counted sequences), written into ``out`` when
-    given."""
+    given.  ``noalloc=True`` calls grpo_surrogate_noalloc (no device
+    allocation in the library; N <= 65536)."""
     import torch
     lib = load_library()
     _dev("new_lp", new_lp, torch.float32, ndim=2)
@@ -398,7 +401,8 @@ def grpo_surrogate(new_lp, old_lp, adv, lengths, G_dev, eps_lo: float = 0.2, eps
     _gpu(new_lp=new_lp, old_lp=old_lp, adv=adv, lengths=lengths, G=G_dev, keep=keep, out=out)
     if out is None:
         out = torch.empty(4, dtype=torch.float64, device=new_lp.device)
-    _check(lib.grpo_surrogate(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()), N, max_new,
+    fn = lib.grpo_surrogate_noalloc if noalloc else lib.grpo_surrogate
+    _check(fn(_ptr(new_lp), _ptr(old_lp), _ptr(adv), _ptr(lengths), _ptr(G_dev), int(G_dev.numel()), N, max_new,
               _ptr(keep), float(eps_lo), float(eps_hi), LOSS_MODES[mode], _ptr(out), _stream_ptr(stream)))
     return out
 

@@ -1083,6 +1083,24 @@ int grpo_surrogate(const float* new_lp, const float* old_lp, const float* adv, c
   return RG_OK;
 }
 
+int grpo_surrogate_noalloc(const float* new_lp, const float* old_lp, const float* adv, const int32_t* lengths,
+                           const int32_t* G, int32_t P, int32_t N, int32_t max_new, const int32_t* keep,
+                           double eps_lo, double eps_hi, int32_t mode, double* out, void* stream) {
+  SurrogateArgs sa;
+  int rc = surrogate_args("grpo_surrogate_noalloc", new_lp, old_lp, adv, lengths, G, P, N, max_new, keep, eps_lo,
+                          eps_hi, mode, out, &sa);
+  if (rc) return rc;
+  if (N > SURROGATE_NOALLOC_MAX_SEQS)
+    return fail(RG_EINVAL, "grpo_surrogate_noalloc: N exceeds the static scratch (" +
+                               std::to_string(SURROGATE_NOALLOC_MAX_SEQS) + " sequences)");
+  SurrogateRec* rec = nullptr;
+  hipError_t e = surrogate_static_scratch(&rec);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("grpo_surrogate_noalloc scratch: ") + hipGetErrorString(e));
+  e = launch_surrogate(sa, rec, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("grpo_surrogate_noalloc launch: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
 int group_advantage(const float* rewards, const int32_t* G, int32_t P, int32_t N, float eps, int32_t ddof, float* adv,
                     void* stream) {
   if (!rewards || !G || !adv) return fail(RG_EINVAL, "group_advantage: NULL argument");

@@ -1,8 +1,18 @@
 // GRPO loss forward: the row set-up of the teacher-forced log-probability
 // recompute over finished rollouts, the per-token log-probability gather
 // after the lm head, and the clipped surrogate reduction.
+#include <mutex>
+#include <vector>
+
 #include "rg_device.h"
 #include "rg_kernels.h"
+
+// Scratch of grpo_surrogate_noalloc: the per-sequence records of up to
+// SURROGATE_NOALLOC_MAX_SEQS sequences (1 MiB), one copy on every device the
+// library runs on, held until the process ends.  Host code never passes this
+// name to a kernel: it uses the device address surrogate_static_scratch()
+// looks up.
+static __device__ __align__(256) SurrogateRec scratch[SURROGATE_NOALLOC_MAX_SEQS];
 
 namespace {
 
@@ -324,6 +334,25 @@ hipError_t launch_token_logprob(const float* logits, int V, float T, const int32
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_token_logprob, dim3(rows), dim3(LP_THREADS), 0, st, logits, V, T, lrow, tgt, out, lp);
   return hipGetLastError();
+}
+
+hipError_t surrogate_static_scratch(SurrogateRec** out) {
+  static std::mutex mu;
+  static std::vector<SurrogateRec*> by_device;   // device address of `scratch`, per device
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)by_device.size() <= dev) by_device.resize(dev + 1, nullptr);
+  if (!by_device[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    by_device[dev] = (SurrogateRec*)ptr;
+  }
+  *out = by_device[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_surrogate(const SurrogateArgs& a, SurrogateRec* rec, hipStream_t st) {

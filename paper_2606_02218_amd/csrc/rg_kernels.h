@@ -294,4 +294,9 @@ static_assert(sizeof(SurrogateRec) == 16, "surrogate record layout");
 // Two launches: per-sequence records into rec [N] (device scratch), then one
 // block that reduces them in a fixed order into a.out.
 hipError_t launch_surrogate(const SurrogateArgs& a, SurrogateRec* rec, hipStream_t st);
-
+// Largest N of grpo_surrogate_noalloc: its records live in a static device
+// array of this many entries (k_loss.hip).
+constexpr int SURROGATE_NOALLOC_MAX_SEQS = 65536;
+// Device address of that array on the current device (looked up with
+// hipGetSymbolAddress on the first call per device, then cached).
+hipError_t surrogate_static_scratch(SurrogateRec** out);
