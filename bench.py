@@ -21,6 +21,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK = 8.0e12            # MI355X HBM3E, bytes/s
 MFMA_BF16_PEAK = 2.5e15      # dense bf16 MFMA, flop/s
+FP32_VALU_PEAK = 157.3e12    # fp32 vector FMA (256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2 packed x 2.4 GHz)
 
 
 def algorithmic_bytes(shape, hist_active, hist_groups, hist_ctx, plen):
@@ -80,11 +81,7 @@ def prefill_flops(shape, plens):
             + 2.0 * V * d * len(n))
 
 
-def cpu_baseline(wl, weights, inputs, n_steps: int):
-    """The oracle on the host: prefill of prompt 0 plus its G siblings for
-    n_steps decode steps (a bounded sample of the same workload)."""
-    from oracle.model import OracleModel
-    from oracle.rollout import rollout as oracle_rollout
+def _oracle_threads() -> int:
     threads = None
     try:
         from threadpoolctl import threadpool_info
@@ -94,15 +91,50 @@ def cpu_baseline(wl, weights, inputs, n_steps: int):
         pass
     if threads is None:
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return int(threads)
+
+
+def cpu_baseline(wl, weights, inputs, n_steps, prompts=(0,)):
+    """The oracle on the host: prefill of the given prompts plus their
+    siblings for n_steps decode steps (n_steps None: to the end; prompts None:
+    every prompt of the workload)."""
+    from oracle.model import OracleModel
+    from oracle.rollout import rollout as oracle_rollout
+    threads = _oracle_threads()
     model = OracleModel(wl.shape, weights)
     t0 = time.perf_counter()
     out = oracle_rollout(model, inputs.prompts, inputs.G, wl.max_new, 1234, inputs.forced_len,
-                         max_steps=n_steps, prompt_subset=[0])
+                         max_steps=n_steps, prompt_subset=None if prompts is None else list(prompts))
     dt = time.perf_counter() - t0
-    gen = int(np.sum(out["tokens"][: int(inputs.G[0])] >= 0))
-    return {"value": gen / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"prompt 0 of the same workload: prefill {wl.prompt_len} tokens + {int(inputs.G[0])} siblings "
-                      f"x {n_steps} decode steps ({gen} tokens) in {dt:.1f} s, float64 numpy"}
+    G = np.asarray(inputs.G, np.int64)
+    off = np.concatenate([[0], np.cumsum(G)])
+    sel = range(len(G)) if prompts is None else prompts
+    gen = int(sum(np.sum(out["tokens"][off[p]:off[p + 1]] >= 0) for p in sel))
+    n_seq = int(sum(G[p] for p in sel))
+    what = "every prompt" if prompts is None else ("prompt " + ", ".join(str(p) for p in sel))
+    steps = "to the end" if n_steps is None else f"x {n_steps} decode steps"
+    return {"value": gen / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{what} of the {wl.name} workload: prefill ({wl.prompt_len}-token prompts) + {n_seq} sequences "
+                      f"{steps} ({gen} tokens) in {dt:.1f} s, float64 numpy"}
+
+
+def cpu_report(args):
+    """The oracle alone (no GPU): the full workload (--cpu-steps 0) or its
+    first --cpu-steps decode steps of prompt 0, optionally on one thread.
+    Prints one JSON line."""
+    from workload import get_config, make_weights, make_inputs
+    wl = get_config(args.workload)
+    weights = make_weights(wl.shape, 0)
+    inp = make_inputs(wl, 0)
+    full = args.cpu_steps == 0
+    if args.cpu_threads:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=args.cpu_threads):
+            r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,))
+    else:
+        r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,))
+    r["workload"] = wl.name
+    print(json.dumps(r), flush=True)
 
 
 def eb_sweep(args):
@@ -349,15 +381,26 @@ def ceilings():
             out.append(e0.elapsed_time(e1))
         return min(out)
 
+    import paper_2606_02218_amd as rg
     res = {"hbm_peak_spec_GBps": HBM_PEAK / 1e9, "mfma_bf16_peak_spec_TFLOPs": MFMA_BF16_PEAK / 1e12}
     n = 1 << 29                                       # 2 GiB of fp32
     a = torch.ones(n, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
     ms = best_ms(lambda: b.copy_(a))
-    res["copy_2GiB"] = {"ms": round(ms, 3), "GBps": round(2 * 4 * n / ms / 1e6, 1)}
+    res["torch_copy_2GiB"] = {"ms": round(ms, 3), "GBps": round(2 * 4 * n / ms / 1e6, 1)}
     ms = best_ms(lambda: a.sum())
-    res["read_sum_2GiB"] = {"ms": round(ms, 3), "GBps": round(4 * n / ms / 1e6, 1)}
-    del a, b
+    res["torch_read_sum_2GiB"] = {"ms": round(ms, 3), "GBps": round(4 * n / ms / 1e6, 1)}
+    # the library's own streaming probe (16-byte loads, grid-stride), by grid size
+    sink = torch.empty(1 << 22, dtype=torch.int32, device="cuda")
+    probe = {}
+    for blocks in (1024, 2048, 4096, 8192, 16384):
+        r_ms = best_ms(lambda: rg.hbm_probe(a, sink, 0, blocks))
+        c_ms = best_ms(lambda: rg.hbm_probe(a, b, 1, blocks))
+        probe[str(blocks)] = {"read_GBps": round(4 * n / r_ms / 1e6, 1), "copy_GBps": round(2 * 4 * n / c_ms / 1e6, 1)}
+    res["probe_2GiB_by_blocks"] = probe
+    res["probe_best"] = {"read_GBps": max(v["read_GBps"] for v in probe.values()),
+                         "copy_GBps": max(v["copy_GBps"] for v in probe.values())}
+    del a, b, sink
     g = {}
     shapes = {"square_8192": (8192, 8192, 8192)}
     for rows in (16384, 512):
@@ -385,6 +428,9 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
     ap.add_argument("--cpu-steps", type=int, default=32, help="decode steps of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-report", action="store_true",
+                    help="only time the oracle on the host (the full workload with --cpu-steps 0) and exit")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="thread limit of the oracle in --cpu-report")
     ap.add_argument("--eb-sweep", type=int, default=0, metavar="T",
                     help="only run the static-G vs controller sweep at EB = 64 with T steps per arm and exit")
     ap.add_argument("--group-prefix", action="store_true",
@@ -399,6 +445,9 @@ def main():
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the HBM copy / read and bf16 GEMM ceilings and exit")
     args = ap.parse_args()
+    if args.cpu_report:
+        cpu_report(args)
+        return
     if args.ceilings:
         ceilings()
         return
@@ -499,7 +548,7 @@ def main():
     res = {"metric": "rollout decode tokens/s (group step = rollout_group + group_advantage)",
            "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_per_step, 2), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-           "dtype": "bf16", "data": "synthetic",
+           "dtype": "bf16" if shape.dtype == "bf16" else "f32", "data": "synthetic",
            "config": {"workload": wl.name, "prompts": wl.n_prompts,
                       "group_size": wl.group_size if wl.group_size is not None else sorted(set(int(g) for g in inp.G)),
                       "sequences": N, "prompt_len": wl.prompt_len, "max_new": wl.max_new,
@@ -512,11 +561,17 @@ def main():
     F = prefill_flops(shape, [wl.prompt_len] * wl.n_prompts)
     res["prefill_ms"] = round(pf_s * 1e3, 2)
     res["decode_s"] = round(dc_s, 4)
-    res["roofline_prefill"] = {"bound": "mfma", "achieved": round(F / pf_s / 1e12, 1), "peak": MFMA_BF16_PEAK / 1e12,
-                               "unit": "TFLOP/s", "frac": round(F / pf_s / MFMA_BF16_PEAK, 4),
-                               "issued_frac": round(2 * F / pf_s / MFMA_BF16_PEAK, 4), "alg_flops": F,
-                               "note": "each fp32 activation enters bf16 MFMA as hi + lo planes: two MFMAs per "
-                                       "product, so the algorithmic fraction is at most half the issued one"}
+    if shape.dtype == "bf16":
+        res["roofline_prefill"] = {"bound": "mfma", "achieved": round(F / pf_s / 1e12, 1),
+                                   "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                                   "frac": round(F / pf_s / MFMA_BF16_PEAK, 4),
+                                   "issued_frac": round(2 * F / pf_s / MFMA_BF16_PEAK, 4), "alg_flops": F,
+                                   "note": "each fp32 activation enters bf16 MFMA as hi + lo planes: two MFMAs per "
+                                           "product, so the algorithmic fraction is at most half the issued one"}
+    else:   # fp32 models run plain fp32 FMA on the vector ALUs
+        res["roofline_prefill"] = {"bound": "alu", "achieved": round(F / pf_s / 1e12, 3),
+                                   "peak": FP32_VALU_PEAK / 1e12, "unit": "TFLOP/s",
+                                   "frac": round(F / pf_s / FP32_VALU_PEAK, 6), "alg_flops": F}
     dec_b = decode_bytes_total(shape, hist_a, hist_g, hist_c)
     res["roofline_decode"] = {"bound": "hbm", "achieved": round(dec_b / dc_s / 1e9, 1), "peak": HBM_PEAK / 1e9,
                               "unit": "GB/s", "frac": round(dec_b / dc_s / HBM_PEAK, 4), "alg_bytes": dec_b,

@@ -310,6 +310,15 @@ int rg_philox_blocks(uint64_t key0, uint64_t key1, const uint64_t* ctr, int64_t 
  * (low first) of 64-bit word ((v&7)>>1).  out is DEVICE uint32 [vocab]. */
 int rg_gumbel_bits(uint64_t seed, int32_t t, int32_t s, int32_t vocab, uint32_t* out, void* stream);
 
+/* Measured streaming ceiling for the HBM rooflines (not a step of the path):
+ * one launch of `blocks` workgroups of 256 threads that stream `bytes` (a
+ * positive multiple of 16) of DEVICE memory at src in 16-byte pieces.
+ * mode 1: copy to DEVICE dst [bytes]; mode 0: read only, one uint32 per
+ * thread stored to DEVICE dst [blocks * 256 * 4 bytes].  src and dst must not
+ * overlap and must be 16-byte aligned.  Enqueue only; RG_EINVAL on a bad
+ * argument. */
+int rg_hbm_probe(const void* src, void* dst, int64_t bytes, int32_t mode, int32_t blocks, void* stream);
+
 /* Per-step record of the last rollout_group call: active[t] = sequences still
  * decoding at step t (t = 0 is the first sampled token), groups[t] = prompts
  * with at least one of them, ctx[t] = sum over those sequences of their prompt

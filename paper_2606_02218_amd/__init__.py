@@ -7,5 +7,5 @@ loudly when the library has not been built.
 """
 from ._lib import (  # noqa: F401
     RolloutError, Policy, group_advantage, philox_blocks, gumbel_bits, lib_path, load_library,
-    KERNEL_KINDS, exported_symbols, Sagc, sagc_beta_draw, group_filter, grpo_surrogate, decode_attention_chunks,
+    KERNEL_KINDS, exported_symbols, Sagc, sagc_beta_draw, group_filter, grpo_surrogate, decode_attention_chunks, hbm_probe,
 )

@@ -19,7 +19,7 @@ KERNEL_KINDS = ["embed", "rmsnorm", "gemm_qkv", "qkv_rope", "attn", "attn_merge"
                 "gemm_down", "residual", "gemm_lm", "sample", "compact", "setup", "logprob"]
 
 EXPORTS = ["rg_last_error", "rg_policy_create", "rg_policy_destroy", "rg_policy_device_bytes", "rollout_group",
-           "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_step_history", "rg_kernel_times",
+           "group_advantage", "rg_philox_blocks", "rg_gumbel_bits", "rg_hbm_probe", "rg_step_history", "rg_kernel_times",
            "sagc_init", "sagc_group_stats", "sagc_step", "sagc_beta_draw", "group_filter",
            "recompute_logprobs", "grpo_surrogate", "rg_decode_attention_chunks", "rg_phase_times",
            "grpo_surrogate_noalloc"]
@@ -120,6 +120,7 @@ def load_library():
                                     C.c_void_p]
     lib.rg_philox_blocks.argtypes = [C.c_uint64, C.c_uint64, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
     lib.rg_gumbel_bits.argtypes = [C.c_uint64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    lib.rg_hbm_probe.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.c_void_p]
     lib.rg_step_history.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rg_kernel_times.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
     lib.group_filter.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -436,6 +437,21 @@ def philox_blocks(key0: int, key1: int, ctr, stream=None):
     _check(lib.rg_philox_blocks(C.c_uint64(key0), C.c_uint64(key1), _ptr(ctr), ctr.shape[0], _ptr(out),
                                 _stream_ptr(stream)))
     return out
+
+
+def hbm_probe(src, dst, mode: int, blocks: int = 2048, stream=None):
+    """One launch of the streaming ceiling probe over the bytes of src (a
+    contiguous device tensor, size a multiple of 16 bytes).  mode 1 copies to
+    dst (same size); mode 0 reads only and dst must hold blocks * 256 int32."""
+    lib = load_library()
+    nbytes = src.numel() * src.element_size()
+    if not src.is_contiguous() or not dst.is_contiguous():
+        raise ValueError("src and dst must be contiguous")
+    need = nbytes if mode == 1 else blocks * 256 * 4
+    if dst.numel() * dst.element_size() < need:
+        raise ValueError(f"dst must hold at least {need} bytes")
+    _gpu(src=src, dst=dst)
+    _check(lib.rg_hbm_probe(_ptr(src), _ptr(dst), C.c_int64(nbytes), mode, blocks, _stream_ptr(stream)))
 
 
 def gumbel_bits(seed: int, t: int, s: int, vocab: int, stream=None):

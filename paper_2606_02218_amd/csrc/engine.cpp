@@ -1136,6 +1136,14 @@ int rg_gumbel_bits(uint64_t seed, int32_t t, int32_t s, int32_t vocab, uint32_t*
   return RG_OK;
 }
 
+int rg_hbm_probe(const void* src, void* dst, int64_t bytes, int32_t mode, int32_t blocks, void* stream) {
+  if (!src || !dst || bytes < 16 || bytes % 16 || (mode != 0 && mode != 1) || blocks < 1 || blocks > (1 << 20))
+    return fail(RG_EINVAL, "rg_hbm_probe: bad argument");
+  hipError_t e = launch_hbm_probe(src, dst, bytes, mode, blocks, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RG_EHIP, std::string("rg_hbm_probe: ") + hipGetErrorString(e));
+  return RG_OK;
+}
+
 int rg_step_history(const rg_policy* pol, int32_t cap, int32_t* n_steps, int32_t* active, int32_t* groups,
                     int64_t* ctx) {
   if (!pol || cap < 0) return fail(RG_EINVAL, "rg_step_history: bad argument");

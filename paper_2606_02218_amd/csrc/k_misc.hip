@@ -53,6 +53,36 @@ __global__ void k_prefill_rows(const int32_t* __restrict__ prompt_off, int P, in
   row_beg[r] = 0;
 }
 
+// Streaming ceiling of the memory system (a measurement aid for the
+// rooflines, not a step of the path): each thread reads four 16-byte pieces
+// per iteration of a grid-stride loop, one grid-stride apart, so every wave
+// reads whole contiguous 1 KB runs.  MODE 1 writes them to dst (a copy);
+// MODE 0 folds them into one word per thread, stored to sink, so the loads
+// stay live (a read).
+typedef uint32_t probe_u32x4 __attribute__((ext_vector_type(4)));
+template <int MODE>
+__global__ __launch_bounds__(256) void k_hbm_probe(const probe_u32x4* __restrict__ src, probe_u32x4* __restrict__ dst,
+                                                   int64_t n16, uint32_t* __restrict__ sink) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const probe_u32x4 v0 = src[i], v1 = src[i + stride], v2 = src[i + 2 * stride], v3 = src[i + 3 * stride];
+    if constexpr (MODE == 1) {
+      dst[i] = v0; dst[i + stride] = v1; dst[i + 2 * stride] = v2; dst[i + 3 * stride] = v3;
+    } else {
+      const probe_u32x4 x = (v0 ^ v1) ^ (v2 ^ v3);
+      acc ^= x.x ^ x.y ^ x.z ^ x.w;
+    }
+  }
+  for (; i < n16; i += stride) {
+    const probe_u32x4 v = src[i];
+    if constexpr (MODE == 1) dst[i] = v;
+    else acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if constexpr (MODE == 0) sink[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
 template <int SPLIT>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, const float* __restrict__ g, int d,
                                                  float eps, ActOut out, const int32_t* __restrict__ src_rows,
@@ -189,5 +219,17 @@ hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, i
 hipError_t launch_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* out, hipStream_t st) {
   const int nb = (vocab + 7) / 8;
   hipLaunchKernelGGL(k_gumbel_bits, dim3((nb + 255) / 256), dim3(256), 0, st, seed, t, s, vocab, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_hbm_probe(const void* src, void* dst, int64_t bytes, int mode, int blocks, hipStream_t st) {
+  if (bytes <= 0) return hipSuccess;
+  const int64_t n16 = bytes / 16;
+  if (mode == 1)
+    hipLaunchKernelGGL(k_hbm_probe<1>, dim3(blocks), dim3(256), 0, st, (const probe_u32x4*)src, (probe_u32x4*)dst, n16,
+                       nullptr);
+  else
+    hipLaunchKernelGGL(k_hbm_probe<0>, dim3(blocks), dim3(256), 0, st, (const probe_u32x4*)src, nullptr, n16,
+                       (uint32_t*)dst);
   return hipGetLastError();
 }

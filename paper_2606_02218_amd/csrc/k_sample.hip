@@ -29,6 +29,8 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
   const int per = (nb + a.n_slices - 1) / a.n_slices;
   const int vb0 = blockIdx.x * per, vb1 = min(nb, vb0 + per);
 
+  // the EOS entry is masked in one 8-token block only
+  const int eos_vb = mask_eos ? (a.eos >> 3) : -1, eos_j = a.eos & 7;
   float best = -INFINITY;
   int best_v = 0x7FFFFFFF;
   float m = -INFINITY, sum = 0.f;
@@ -38,23 +40,31 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
     rg_u64x4 w = rg_philox4x64_10(c, a.seed, RG_TAG_GUMBEL);
     const float4 z0 = *reinterpret_cast<const float4*>(z + vb * 8);
     const float4 z1 = *reinterpret_cast<const float4*>(z + vb * 8 + 4);
-    const float zz[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+    float zt[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+    if (!unit_T) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) zt[j] /= T;                // z / 1 == z exactly: skipped at T = 1
+    }
+    // running logsumexp, rescaled once per 8 tokens (hardware exponential,
+    // relative error ~1e-7)
+    float bm = zt[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) bm = fmaxf(bm, zt[j]);
+    if (bm > m) { sum *= __expf(m - bm); m = bm; }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += __expf(zt[j] - m);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int v = vb * 8 + j;
-      const float zt = unit_T ? zz[j] : zz[j] / T;
-      // running logsumexp: the hardware exponential (relative error ~1e-7)
-      if (zt > m) { sum = sum * __expf(m - zt) + 1.f; m = zt; }
-      else sum += __expf(zt - m);
       const uint32_t bits = (uint32_t)(w.v[j >> 1] >> (32 * (j & 1)));
       const float u = rg_uniform_from_bits(bits);
       // Gumbel noise -log(-log u): the inner log keeps full accuracy (for u
       // near 1 its result is ~6e-8, where only a relative-error log is safe);
       // the outer one takes an argument in [6e-8, 16.7] and needs ~1e-7
       // absolute accuracy, which the hardware logarithm gives
-      float sc = zt + (-__logf(-logf(u)));
-      if (mask_eos && v == a.eos) sc = -INFINITY;
-      if (sc > best || (sc == best && v < best_v)) { best = sc; best_v = v; }
+      float sc = zt[j] + (-__logf(-logf(u)));
+      if (vb == eos_vb && j == eos_j) sc = -INFINITY;
+      // a thread scans increasing ids, so a strict > keeps the lowest id of a tie
+      if (sc > best) { best = sc; best_v = vb * 8 + j; }
     }
     if (a.dump_logits && t < a.dump_steps) {
       float* dst = a.dump_logits + ((int64_t)t * a.n_seq + s) * a.V + vb * 8;
@@ -86,25 +96,38 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_sample_slice(SampleArgs a) {
   }
 }
 
+// One wave per row: lane l combines slices l, l + 64, ... in order, then the
+// lanes' results are combined across the wave (best score, ties to the
+// lowest id; logsumexp by max and rescaled sums).
 __global__ __launch_bounds__(64) void k_sample_pick(SampleArgs a) {
   const int r = blockIdx.x;
-  if (r >= *a.d_rows || threadIdx.x != 0) return;
+  if (r >= *a.d_rows) return;
+  const int lane = threadIdx.x;
+  float best = -INFINITY, m = -INFINITY, sum = 0.f;
+  int y = 0x7FFFFFFF;
+  for (int k = lane; k < a.n_slices; k += 64) {
+    const float4 p = *reinterpret_cast<const float4*>(a.part + ((int64_t)r * a.n_slices + k) * 4);
+    const int v2 = __float_as_int(p.y);
+    if (p.x > best || (p.x == best && v2 < y)) { best = p.x; y = v2; }
+    const float mm = fmaxf(m, p.z);
+    sum = (m == -INFINITY ? 0.f : sum * expf(m - mm)) + (p.z == -INFINITY ? 0.f : p.w * expf(p.z - mm));
+    m = mm;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float b2 = __shfl_xor(best, o, 64), m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(sum, o, 64);
+    const int v2 = __shfl_xor(y, o, 64);
+    if (b2 > best || (b2 == best && v2 < y)) { best = b2; y = v2; }
+    const float mm = fmaxf(m, m2);
+    sum = (m == -INFINITY ? 0.f : sum * expf(m - mm)) + (m2 == -INFINITY ? 0.f : s2 * expf(m2 - mm));
+    m = mm;
+  }
+  if (lane != 0) return;
   const int t = *a.d_t;
   const int s = a.act_seq[r];
   const int lrow = a.logits_by_group ? a.seq_grp[s] : r;
   const float* z = a.logits + (int64_t)lrow * a.V;
   const int L = a.forced_len ? a.forced_len[s] : -1;
-  float best = -INFINITY, m = -INFINITY, sum = 0.f;
-  int y = 0x7FFFFFFF;
-  for (int k = 0; k < a.n_slices; ++k) {
-    const float* p = a.part + ((int64_t)r * a.n_slices + k) * 4;
-    const float b2 = p[0];
-    const int v2 = __float_as_int(p[1]);
-    if (b2 > best || (b2 == best && v2 < y)) { best = b2; y = v2; }
-    const float mm = fmaxf(m, p[2]);
-    sum = (m == -INFINITY ? 0.f : sum * expf(m - mm)) + (p[2] == -INFINITY ? 0.f : p[3] * expf(p[2] - mm));
-    m = mm;
-  }
   if (L > 0 && t == L - 1) y = a.eos;
   int fed = a.force_tokens ? a.force_tokens[(int64_t)s * a.max_new + t] : y;
   if (fed < 0 || fed >= a.V) { fed = a.eos; a.bad_token[0] = 1; }   // invalid forced id: stop this sequence

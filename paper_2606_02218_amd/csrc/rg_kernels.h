@@ -233,6 +233,9 @@ hipError_t launch_group_advantage(const float* rewards, const int32_t* G, int P,
 hipError_t launch_philox_blocks(uint64_t k0, uint64_t k1, const uint64_t* ctr, int64_t n, uint64_t* out,
                                 hipStream_t st);
 hipError_t launch_gumbel_bits(uint64_t seed, int t, int s, int vocab, uint32_t* out, hipStream_t st);
+// Streaming ceiling probe: mode 1 copies `bytes` from src to dst, mode 0 only
+// reads src and stores one word per thread (blocks*256 words) to dst.
+hipError_t launch_hbm_probe(const void* src, void* dst, int64_t bytes, int mode, int blocks, hipStream_t st);
 
 // ---- GRPO loss forward (k_loss.hip)
 // After the fork: per-sequence row offsets of the teacher-forced forward

@@ -3,6 +3,7 @@
     python -m paper_2606_02218_amd.prof stats DIR              # per-kernel time table
     python -m paper_2606_02218_amd.prof trace DIR [TOP]        # per kernel and grid size, from kernel_trace.csv
     python -m paper_2606_02218_amd.prof steps DIR              # decode-step time by active-row bucket
+    python -m paper_2606_02218_amd.prof steps-full DIR         # the same, every kernel instantiation listed
     python -m paper_2606_02218_amd.prof phases DIR HIST.npz    # decode attention by phase of one rollout
     python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
 """
@@ -65,25 +66,29 @@ def _kname(r) -> str:
     return _short(r.get("Kernel_Name", "?")).split("(")[0].split("<")[0]
 
 
-def steps_table(d: str) -> str:
+def steps_table(d: str, full: bool = False) -> str:
     """Decode steps delimited by k_compact; a step's row bound comes from the
     grid of its k_decode_rows launch (one 256-thread block per row).  Reports,
     per row bucket, the steps, GPU-busy and wall span per step, and the busy
-    time per kernel name."""
+    time per kernel name (full: per template instantiation, with launches
+    per step and the mean launch duration)."""
     rows = []
     for f in _find(d, "kernel_trace.csv"):
         rows += list(csv.DictReader(open(f)))
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     buckets = collections.OrderedDict((b, None) for b in (16, 32, 64, 128, 256, 384, 512, 1 << 30))
     acc = {b: {"steps": 0, "busy": 0.0, "span": 0.0, "k": collections.Counter()} for b in buckets}
+    cnt, cur_n = collections.Counter(), collections.Counter()
     cur, m, t0, busy = collections.Counter(), None, None, 0.0
     for r in rows:
         name = _kname(r)
+        key = _short(r.get("Kernel_Name", "?")).split("(")[0] if full else name
         s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
         if t0 is None:
             t0 = s0
         dur = (e0 - s0) / 1e3
-        cur[name] += dur
+        cur[key] += dur
+        cur_n[key] += 1
         busy += dur
         if name == "k_decode_rows":
             m = int(r.get("Grid_Size_X", "0") or 0) // 256
@@ -95,7 +100,8 @@ def steps_table(d: str) -> str:
                 a["busy"] += busy
                 a["span"] += (e0 - t0) / 1e3
                 a["k"].update(cur)
-            cur, m, t0, busy = collections.Counter(), None, None, 0.0
+                a.setdefault("n", collections.Counter()).update(cur_n)
+            cur, cur_n, m, t0, busy = collections.Counter(), collections.Counter(), None, None, 0.0
     out = [f"{'rows<=':>8s} {'steps':>6s} {'busy_ms/step':>13s} {'span_ms/step':>13s} {'total_span_s':>13s}  top kernels (us/step)"]
     for b, a in acc.items():
         if not a["steps"]:
@@ -103,7 +109,11 @@ def steps_table(d: str) -> str:
         n = a["steps"]
         top = ", ".join(f"{k} {v / n:.0f}" for k, v in a["k"].most_common(6))
         out.append(f"{b if b < (1 << 30) else 'more':>8} {n:6d} {a['busy'] / n / 1e3:13.3f} {a['span'] / n / 1e3:13.3f} "
-                   f"{a['span'] / 1e6:13.2f}  {top}")
+                   f"{a['span'] / 1e6:13.2f}" + ("" if full else f"  {top}"))
+        if full:
+            for k, v in a["k"].most_common():
+                c = a["n"][k]
+                out.append(f"{'':>8} {k[:70]:70s} {c / n:7.1f}/step {v / n:9.1f} us/step {v / c:8.2f} us")
     return "\n".join(out)
 
 
@@ -188,6 +198,8 @@ if __name__ == "__main__":
         print(trace_table(sys.argv[2], int(sys.argv[3]) if len(sys.argv) > 3 else 60))
     elif len(sys.argv) >= 3 and sys.argv[1] == "steps":
         print(steps_table(sys.argv[2]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "steps-full":
+        print(steps_table(sys.argv[2], full=True))
     elif len(sys.argv) >= 4 and sys.argv[1] == "phases":
         print(phases_table(sys.argv[2], sys.argv[3]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
