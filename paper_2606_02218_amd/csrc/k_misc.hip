@@ -54,30 +54,33 @@ __global__ void k_prefill_rows(const int32_t* __restrict__ prompt_off, int P, in
 }
 
 // Streaming ceiling of the memory system (a measurement aid for the
-// rooflines, not a step of the path): each thread reads four 16-byte pieces
+// rooflines, not a step of the path): each thread reads eight 16-byte pieces
 // per iteration of a grid-stride loop, one grid-stride apart, so every wave
-// reads whole contiguous 1 KB runs.  MODE 1 writes them to dst (a copy);
-// MODE 0 folds them into one word per thread, stored to sink, so the loads
-// stay live (a read).
+// reads whole contiguous 1 KB runs, with non-temporal loads (and stores)
+// that do not claim cache space.  MODE 1 writes them to dst (a copy); MODE 0
+// folds them into one word per thread, stored to sink, so the loads stay
+// live (a read).
 typedef uint32_t probe_u32x4 __attribute__((ext_vector_type(4)));
 template <int MODE>
 __global__ __launch_bounds__(256) void k_hbm_probe(const probe_u32x4* __restrict__ src, probe_u32x4* __restrict__ dst,
                                                    int64_t n16, uint32_t* __restrict__ sink) {
+  constexpr int U = 8;
   const int64_t stride = (int64_t)gridDim.x * 256;
   int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   uint32_t acc = 0;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const probe_u32x4 v0 = src[i], v1 = src[i + stride], v2 = src[i + 2 * stride], v3 = src[i + 3 * stride];
-    if constexpr (MODE == 1) {
-      dst[i] = v0; dst[i + stride] = v1; dst[i + 2 * stride] = v2; dst[i + 3 * stride] = v3;
-    } else {
-      const probe_u32x4 x = (v0 ^ v1) ^ (v2 ^ v3);
-      acc ^= x.x ^ x.y ^ x.z ^ x.w;
+  for (; i + (U - 1) * stride < n16; i += U * stride) {
+    probe_u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * stride]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if constexpr (MODE == 1) __builtin_nontemporal_store(v[u], &dst[i + u * stride]);
+      else acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
     }
   }
   for (; i < n16; i += stride) {
-    const probe_u32x4 v = src[i];
-    if constexpr (MODE == 1) dst[i] = v;
+    const probe_u32x4 v = __builtin_nontemporal_load(&src[i]);
+    if constexpr (MODE == 1) __builtin_nontemporal_store(v, &dst[i]);
     else acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
   if constexpr (MODE == 0) sink[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc;
