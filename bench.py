@@ -444,6 +444,9 @@ def main():
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the HBM copy / read and bf16 GEMM ceilings and exit")
+    ap.add_argument("--prefill-probe", type=int, default=0, metavar="K",
+                    help="only run K rollouts of the workload's prompts with every completion forced to 2 tokens "
+                         "(the prefill and one full-batch decode step; a short command for counter passes) and exit")
     args = ap.parse_args()
     if args.cpu_report:
         cpu_report(args)
@@ -487,6 +490,18 @@ def main():
     print(f"# policy ready: {pol.device_bytes() / 2**30:.1f} GiB on the device", file=sys.stderr, flush=True)
     dev = torch.device("cuda")
     prompts = torch.from_numpy(inp.prompts).to(dev)
+    if args.prefill_probe:
+        two = np.full(N, 2, dtype=np.int32)
+        out = (torch.empty((N, 2), dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.int32, device=dev),
+               torch.empty((N, 2), dtype=torch.float32, device=dev))
+        pf = []
+        for i in range(args.prefill_probe):
+            pol.rollout(prompts, inp.G, 2, 1234 + i, forced_len=two, out=out)
+            pf.append(pol.phase_times()[0])
+        torch.cuda.synchronize()
+        print(json.dumps({"prefill_probe": wl.name, "rollouts": args.prefill_probe, "prefill_ms": [round(v, 2) for v in pf],
+                          "prefill_flops": prefill_flops(shape, [wl.prompt_len] * wl.n_prompts)}), flush=True)
+        return
     G_dev = torch.from_numpy(inp.G).to(dev)
     rewards = torch.from_numpy(inp.rewards).to(dev)
     tokens = torch.empty((N, wl.max_new), dtype=torch.int32, device=dev)

@@ -6,6 +6,7 @@
     python -m paper_2606_02218_amd.prof steps-full DIR         # the same, every kernel instantiation listed
     python -m paper_2606_02218_amd.prof phases DIR HIST.npz    # decode attention by phase of one rollout
     python -m paper_2606_02218_amd.prof counters DIR REGEX     # mean counter per dispatch
+    python -m paper_2606_02218_amd.prof step-counters DIR      # counters per kernel and decode-row bucket
 """
 from __future__ import annotations
 
@@ -191,6 +192,61 @@ def counter_table(d: str, regex: str) -> str:
     return "\n".join(out)
 
 
+def step_counters(d: str) -> dict:
+    """Counter collection grouped like `steps`: dispatches before the first
+    k_decode_rows are the prefill; after it, decode steps are delimited by
+    k_compact and bucketed by the row bound of their k_decode_rows launch.
+    Returns {bucket: {kernel: {"dispatches": n, counter: sum}}}."""
+    disp = {}
+    for f in _find(d, "counter_collection.csv"):
+        for r in csv.DictReader(open(f)):
+            key = (f, int(r["Dispatch_Id"]))
+            e = disp.get(key)
+            if e is None:
+                e = disp[key] = {"t": int(r.get("Start_Timestamp", 0) or 0), "name": r.get("Kernel_Name", "?"),
+                                 "grid": int(r.get("Grid_Size", 0) or 0), "c": collections.Counter()}
+            e["c"][r["Counter_Name"]] += float(r.get("Counter_Value", 0) or 0)
+    order = sorted(disp.values(), key=lambda e: e["t"])
+    buckets = (16, 32, 64, 128, 256, 384, 512, 1 << 30)
+    out = collections.OrderedDict()
+    cur, m, decoding = [], None, False
+
+    def flush(label):
+        b = out.setdefault(label, {})
+        for e in cur:
+            k = b.setdefault(_short(e["name"]).split("(")[0], collections.Counter())
+            k["dispatches"] += 1
+            k.update(e["c"])
+
+    for e in order:
+        name = _short(e["name"]).split("(")[0].split("<")[0]
+        if name == "k_decode_rows" and not decoding:
+            flush("prefill")
+            cur, decoding = [], True
+        cur.append(e)
+        if name == "k_decode_rows":
+            m = e["grid"] // 256
+        if decoding and name == "k_compact" and m is not None:
+            flush(str(next(b for b in buckets if m <= b)))
+            cur, m = [], None
+    if cur:
+        flush("prefill" if not decoding else "tail")
+    return out
+
+
+def step_counters_table(d: str) -> str:
+    res = step_counters(d)
+    lines = []
+    for b, ks in res.items():
+        lines.append(f"[{b}]")
+        names = sorted({c for k in ks.values() for c in k if c != "dispatches"})
+        lines.append(f"  {'kernel':64s} {'dispatches':>10s} " + " ".join(f"{c:>26s}" for c in names))
+        for k, v in sorted(ks.items(), key=lambda kv: -kv[1]["dispatches"]):
+            n = v["dispatches"]
+            lines.append(f"  {k[:64]:64s} {n:10d} " + " ".join(f"{v[c] / n:26.1f}" for c in names))
+    return "\n".join(lines)
+
+
 if __name__ == "__main__":
     if len(sys.argv) >= 3 and sys.argv[1] == "stats":
         print(stats_table(sys.argv[2]))
@@ -204,6 +260,8 @@ if __name__ == "__main__":
         print(phases_table(sys.argv[2], sys.argv[3]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
         print(counter_table(sys.argv[2], sys.argv[3]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "step-counters":
+        print(step_counters_table(sys.argv[2]))
     else:
         print(__doc__)
         sys.exit(2)

@@ -54,3 +54,38 @@ def test_phases_table(tmp_path):
     assert int(small[1]) == L and float(small[2]) == 8.0 and float(small[3]) == 2.0
     assert abs(float(small[6]) - alg2 / (4 * ms) / 1e3) < 0.006
     assert out[-1] == "total: attention 28.0 ms, merge 2.0 ms"
+
+
+def _counters(path, dispatches):
+    cols = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp"]
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=cols)
+        w.writeheader()
+        for i, (name, grid, cnt) in enumerate(dispatches):
+            for c, v in cnt.items():
+                w.writerow({"Dispatch_Id": i + 1, "Grid_Size": grid, "Kernel_Name": name, "Counter_Name": c,
+                            "Counter_Value": v, "Start_Timestamp": 100 * i})
+
+
+def test_step_counters(tmp_path):
+    """Dispatches before the first decode-row set-up are the prefill; each
+    decode step (closed by k_compact) lands in the bucket of its row bound
+    (the k_decode_rows grid / 256); counters are summed per kernel."""
+    from paper_2606_02218_amd.prof import step_counters
+    g = "void k_gemm_tiled<32, 128, 1, 4, 1, 64, 4, true>(x)"
+    rows = "void k_decode_rows<unsigned short>(int)"
+    comp = "void k_compact(int)"
+    disp = [("void k_gemm_tiled<256, 256, 4, 8, 1, 64, 2, false>(x)", 9, {"A": 10.0}),
+            ("void k_gemm_tiled<256, 256, 4, 8, 1, 64, 2, false>(x)", 9, {"A": 30.0})]
+    for m in (20, 20, 300):                 # two steps at <= 32 rows, one at <= 384
+        disp += [(rows, 256 * m, {"A": 1.0}), (g, 7, {"A": float(m)}), (comp, 1024, {"A": 0.0})]
+    os.makedirs(tmp_path / "pmc" / "x")
+    _counters(tmp_path / "pmc" / "x" / "run_counter_collection.csv", disp)
+    res = step_counters(str(tmp_path / "pmc"))
+    assert list(res) == ["prefill", "32", "384"]
+    pre = res["prefill"]["k_gemm_tiled<256, 256, 4, 8, 1, 64, 2, false>"]
+    assert pre["dispatches"] == 2 and pre["A"] == 40.0
+    k32 = res["32"]["k_gemm_tiled<32, 128, 1, 4, 1, 64, 4, true>"]
+    assert k32["dispatches"] == 2 and k32["A"] == 40.0
+    assert res["384"]["k_gemm_tiled<32, 128, 1, 4, 1, 64, 4, true>"]["A"] == 300.0
+    assert res["32"]["k_compact"]["dispatches"] == 2
