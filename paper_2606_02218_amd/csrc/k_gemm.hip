@@ -201,6 +201,8 @@ __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, i
 // block of the launch reads (one row tile): streamed through without
 // claiming cache space, which measured 6.5-6.7 TB/s against 5.9-6.1 TB/s
 // for plain loads in a pure streaming read of 8 GiB.
+__device__ __forceinline__ int k_split_count(int K, int k_per_split) { return (K + k_per_split - 1) / k_per_split; }
+
 template <bool NT>
 __device__ __forceinline__ u32x4_t load_w(const bf16_t* p) {
   if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
@@ -210,7 +212,7 @@ __device__ __forceinline__ u32x4_t load_w(const bf16_t* p) {
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
-    const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep) {
+    const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy) {
   constexpr int WAVES_M = BM / (16 * WM), WAVES_N = BN / (16 * WN);
   constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int LROW = BK + LDS_PAD;                // LDS row stride (elements)
@@ -224,11 +226,32 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LROW];
   __shared__ __attribute__((aligned(16))) bf16_t sW[BN * LROW];
 
+  int tx = blockIdx.x, ty = blockIdx.y, tz = blockIdx.z;
+  if constexpr (BM == 256) {
+    // Large row counts (256 x 256 tiles): a 1-D grid of a multiple of 8
+    // blocks, dealt to the 8 XCDs in turn.  XCD x = b % 8 takes the
+    // contiguous tile range [x*per, (x+1)*per) (split-major), walked in
+    // groups of TILE_GROUP row tiles: within a group, the row tiles of one
+    // column tile are consecutive, so the blocks that an XCD runs at once
+    // share A rows and W columns in its L2.
+    constexpr int TILE_GROUP = 4;
+    const int per = gridDim.x / 8;
+    int w = (blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (w >= gx * gy * (int)k_split_count(K, k_per_split)) return;
+    tz = w / (gx * gy);
+    w -= tz * gx * gy;
+    const int gsz = TILE_GROUP * gx;                    // tiles per full group
+    const int g = w / gsz, r0 = g * TILE_GROUP;
+    const int rows_g = min(TILE_GROUP, gy - r0);       // the last group may be short
+    const int wi = w - g * gsz;
+    ty = r0 + wi % rows_g;
+    tx = wi / rows_g;
+  }
   const int M = *d_rows;
-  const int m0 = blockIdx.y * BM;
+  const int m0 = ty * BM;
   if (m0 >= M) return;
-  const int n0 = blockIdx.x * BN;
-  const int kb0 = blockIdx.z * k_per_split;
+  const int n0 = tx * BN;
+  const int kb0 = tz * k_per_split;
   const int ke = min(K, kb0 + k_per_split);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -304,7 +327,7 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
 #undef RG_STASH
 
   if constexpr (EPI == GEMM_EPI_PARTIAL) {
-    float* pp = ep.part + blockIdx.z * ep.part_stride;
+    float* pp = ep.part + tz * ep.part_stride;
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -443,20 +466,25 @@ template <int BM, int BN, int WM, int WN, int STAGES, int BK = 64>
 hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, int ldw, const int* d_rows,
                         int rows_ub, int N, int K, int splits, int k_per_split, const GemmEpi& ep, hipStream_t st) {
   constexpr int NT = (BM / (16 * WM)) * (BN / (16 * WN)) * 64;
-  dim3 grid((N + BN - 1) / BN, (rows_ub + BM - 1) / BM, splits);
+  const int gx = (N + BN - 1) / BN, gy = (rows_ub + BM - 1) / BM;
+  dim3 grid(gx, gy, splits);
+  if (BM == 256) {
+    if ((K + k_per_split - 1) / k_per_split != splits) return hipErrorInvalidValue;
+    grid = dim3((unsigned)(((int64_t)gx * gy * splits + 7) / 8 * 8));
+  }
   // One row tile: every weight piece is read by one block only, so its loads
   // are non-temporal.  With several row tiles the weight tiles are re-read
   // by the other row tiles' blocks through L2, and non-temporal loads there
   // measured 12 % slower over the 1.5B group step.
-  const bool ntw = grid.y == 1;
+  const bool ntw = gy == 1;
 #define RG_TILED(E)                                                                                           \
   do {                                                                                                        \
     if (ntw)                                                                                                  \
       hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, true>), grid, dim3(NT), 0, st,         \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep); \
+                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep, gx, gy); \
     else                                                                                                      \
       hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, false>), grid, dim3(NT), 0, st,        \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep); \
+                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep, gx, gy); \
   } while (0)
   if (splits > 1) {
     RG_TILED(GEMM_EPI_PARTIAL);
