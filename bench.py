@@ -94,7 +94,7 @@ def _oracle_threads() -> int:
     return int(threads)
 
 
-def cpu_baseline(wl, weights, inputs, n_steps, prompts=(0,)):
+def cpu_baseline(wl, weights, inputs, n_steps, prompts=(0,), progress=0):
     """The oracle on the host: prefill of the given prompts plus their
     siblings for n_steps decode steps (n_steps None: to the end; prompts None:
     every prompt of the workload)."""
@@ -103,8 +103,13 @@ def cpu_baseline(wl, weights, inputs, n_steps, prompts=(0,)):
     threads = _oracle_threads()
     model = OracleModel(wl.shape, weights)
     t0 = time.perf_counter()
+    def on_step(p, t, n):
+        if progress and t % progress == 0:
+            print(f"# oracle prompt {p} step {t}: {n} sequences decoding", file=sys.stderr, flush=True)
+
     out = oracle_rollout(model, inputs.prompts, inputs.G, wl.max_new, 1234, inputs.forced_len,
-                         max_steps=n_steps, prompt_subset=None if prompts is None else list(prompts))
+                         max_steps=n_steps, prompt_subset=None if prompts is None else list(prompts),
+                         on_step=on_step)
     dt = time.perf_counter() - t0
     G = np.asarray(inputs.G, np.int64)
     off = np.concatenate([[0], np.cumsum(G)])
@@ -130,9 +135,9 @@ def cpu_report(args):
     if args.cpu_threads:
         from threadpoolctl import threadpool_limits
         with threadpool_limits(limits=args.cpu_threads):
-            r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,))
+            r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,), progress=16)
     else:
-        r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,))
+        r = cpu_baseline(wl, weights, inp, None if full else args.cpu_steps, None if full else (0,), progress=16)
     r["workload"] = wl.name
     print(json.dumps(r), flush=True)
 

@@ -23,10 +23,13 @@ def group_offsets(G) -> np.ndarray:
 
 
 def rollout(model: OracleModel, prompts, G, max_new: int, seed: int, forced_len=None,
-            temperature: float = 1.0, max_steps=None, prompt_subset=None, record_steps: int = 0):
+            temperature: float = 1.0, max_steps=None, prompt_subset=None, record_steps: int = 0,
+            on_step=None):
     """Free-running rollout.  ``max_steps`` truncates generation (sequences not
     yet retired keep length 0); ``prompt_subset`` restricts it to some prompts;
-    ``record_steps`` keeps the logits of steps t < record_steps.
+    ``record_steps`` keeps the logits of steps t < record_steps; ``on_step``, if
+    given, is called as on_step(p, t, n_active) after each decode step (a
+    progress hook for long timings; it sees no values of the computation).
 
     Returns a dict with tokens [N, max_new] int32, lengths [N] int32, logprobs
     [N, max_new] float64, margins [N, max_new] float64 (nan where not sampled)
@@ -69,6 +72,8 @@ def rollout(model: OracleModel, prompts, G, max_new: int, seed: int, forced_len=
                                         [caches[s] for s in still])
                 z = {s: zz[i] for i, s in enumerate(still)}
             active = still
+            if on_step is not None:
+                on_step(p, t, len(active))
     out = dict(tokens=tokens, lengths=lengths, logprobs=logprobs, margins=margins)
     if record_steps:
         out["logits"] = logits

@@ -124,3 +124,16 @@ def test_recompute_checks_every_buffer_before_the_device():
         pol.recompute_logprobs(pr, [2, 1], tok.long(), torch.ones(3, dtype=torch.int32))
     with pytest.raises(ValueError, match="logprobs"):
         pol.recompute_logprobs(pr, [2, 1], tok, torch.ones(3, dtype=torch.int32), out=torch.zeros((3, 5)))
+
+
+def test_hbm_probe_rejects_bad_inputs():
+    from paper_2606_02218_amd import _lib
+    src = torch.zeros(64, dtype=torch.int32)
+    with pytest.raises(ValueError, match="contiguous"):
+        _lib.hbm_probe(torch.zeros((8, 8), dtype=torch.int32).t(), src, 1)
+    with pytest.raises(ValueError, match="at least"):
+        _lib.hbm_probe(src, torch.zeros(16, dtype=torch.int32), 1)
+    with pytest.raises(ValueError, match="at least"):
+        _lib.hbm_probe(src, torch.zeros(64, dtype=torch.int32), 0, blocks=1)
+    with pytest.raises(TypeError, match="GPU memory"):
+        _lib.hbm_probe(src, torch.zeros(64, dtype=torch.int32), 1)

@@ -135,3 +135,27 @@ def test_group_filter_bad_group_sizes(rg):
         keep, ids, n = rg.group_filter(r, torch.tensor(G, dtype=torch.int32, device="cuda"))
         assert int(n.item()) == -1, G
         assert np.all(ids.cpu().numpy() == -1), G
+
+
+@pytest.mark.parametrize("n16,blocks", [(1, 1), (257, 3), (4096 * 33 + 5, 64), (1 << 20, 2048)])
+def test_hbm_probe_copy_and_read(rg, n16, blocks):
+    """The streaming ceiling probe (a measurement hook, not a path step):
+    mode 1 copies every 16-byte piece, including the grid-stride tail;
+    mode 0 stores, per thread, the xor of every word it read."""
+    import torch
+    g = torch.Generator().manual_seed(n16)
+    src = torch.randint(-2 ** 31, 2 ** 31 - 1, (n16 * 4,), dtype=torch.int32, generator=g).cuda()
+    dst = torch.zeros_like(src)
+    rg.hbm_probe(src, dst, 1, blocks)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
+    rg.hbm_probe(src, sink, 0, blocks)
+    torch.cuda.synchronize()
+    # thread i of the grid reads pieces i, i + T, i + 2T, ... (T = blocks * 256 threads)
+    words = src.cpu().numpy().view(np.uint32).reshape(n16, 4)
+    T = blocks * 256
+    expect = np.zeros(T, np.uint32)
+    for i in range(min(T, n16)):
+        expect[i] = np.bitwise_xor.reduce(words[i::T].reshape(-1))
+    np.testing.assert_array_equal(sink.cpu().numpy().view(np.uint32), expect)
