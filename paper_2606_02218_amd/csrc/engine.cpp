@@ -352,7 +352,8 @@ int run_layers(rg_policy* pol, hipStream_t st, const int* d_rows, int rows_ub, i
     LAUNCH_TIMED(RG_K_ATTN, launch_attention(pol->dtype, pol->qbuf, pol->nq, pol->nkv, pol->hd, pol->kv_pool, pol->geom, l,
                                        pol->page_tab, tab_stride, pol->row_tab, pol->row_pos, pol->row_beg, ctx_max,
                                        plan, pol->att_o, pol->att_ml, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
-    if (plan.n_slots > 1 || pol->dtype != RG_DTYPE_BF16)   // one bf16 slot: the attention wrote abuf2 itself
+    // one bf16 slot, or chunks merged inside the attention kernel: it wrote abuf2 itself
+    if ((plan.n_slots > 1 && !att_merges_in_kernel(pol->dtype, plan, rows_ub, pol->nkv)) || pol->dtype != RG_DTYPE_BF16)
       LAUNCH(RG_K_ATTN_MERGE, launch_attn_merge(pol->dtype, pol->att_o, pol->att_ml, pol->nq, pol->hd, pol->row_pos,
                                                 pol->row_beg, plan, pol->abuf2, pol->a_plane, d_rows, rows_ub, st));
     }

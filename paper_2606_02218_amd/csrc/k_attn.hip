@@ -350,8 +350,12 @@ __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restri
   for (int dt = 0; dt < HD / 16; ++dt) b.v[dt] = *reinterpret_cast<const u32x4_t*>(vp + dt * 16 * 8);
 }
 
-template <int HD, int NB>
-__global__ __launch_bounds__(64, NB > 2 ? 1 : 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
+// W > 1: one workgroup of W waves per (row, kv head), wave c taking context
+// chunk c of the row's W chunks; at the end the waves merge their (max, sum,
+// output) states through LDS in chunk order and write the normalised
+// activation, so no merge kernel runs.
+template <int HD, int NB, int W>
+__global__ __launch_bounds__(64 * W, NB > 2 ? 1 : 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
                                                        const bf16_t* __restrict__ pool, KvGeom g, int layer,
                                                        const int32_t* __restrict__ page_tab, int tab_stride,
                                                        const int32_t* __restrict__ row_tab,
@@ -366,25 +370,36 @@ __global__ __launch_bounds__(64, NB > 2 ? 1 : 2) void k_attention_mfma(const flo
   // work range [x*per_xcd, (x+1)*per_xcd): neighbouring rows (siblings of one
   // prompt) share an XCD, whose L2 then holds their shared prefix.
   const int n_chunks = plan.n_chunks;
-  const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
   const int64_t b = blockIdx.x;
   const int64_t per_xcd = (int64_t)gridDim.x / 8;
   const int64_t w = (b % 8) * per_xcd + b / 8;
-  if (w >= nb) return;
-  const int chunk = (int)(w % n_chunks);
-  const int kvh = (int)((w / n_chunks) % n_kv);
-  const int r = (int)(w / ((int64_t)n_chunks * n_kv));
-  if (r >= *d_rows) return;
+  const int wave = W == 1 ? 0 : (int)(threadIdx.x >> 6);
+  int chunk, kvh, r;
+  if constexpr (W == 1) {
+    if (w >= (int64_t)n_chunks * n_kv * rows_ub) return;
+    chunk = (int)(w % n_chunks);
+    kvh = (int)((w / n_chunks) % n_kv);
+    r = (int)(w / ((int64_t)n_chunks * n_kv));
+  } else {   // the workgroup's (row, kv head); n_chunks == W
+    if (w >= (int64_t)n_kv * rows_ub) return;
+    chunk = wave;
+    kvh = (int)(w % n_kv);
+    r = (int)(w / n_kv);
+  }
+  if (r >= *d_rows) return;                         // uniform over the workgroup
   const int ctx = row_pos[r] + 1, beg = row_beg[r];
   const int clen = att_chunk_len(ctx - beg, n_chunks);
   const int c0 = beg + chunk * clen;                // a multiple of 16
-  if (c0 >= ctx) return;
-  const int c1 = min(ctx, c0 + clen);
+  if constexpr (W == 1)
+    if (c0 >= ctx) return;
+  const bool live = c0 < ctx;                       // W > 1: an empty chunk still joins the merge
+  const int c1 = live ? min(ctx, c0 + clen) : c0;
   const int rep = n_q / n_kv;
-  const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
+  const int lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
 
-  // page ids of the chunk, once
-  __shared__ int spg[ATT_MAX_CHUNK_PAGES];
+  // page ids of the chunk, once (each wave its own)
+  __shared__ int spg_w[W][ATT_MAX_CHUNK_PAGES];
+  int* spg = spg_w[wave];
   {
     const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride + (c0 >> 4);
     const int npg = (c1 - c0 + 15) >> 4;
@@ -397,10 +412,11 @@ __global__ __launch_bounds__(64, NB > 2 ? 1 : 2) void k_attention_mfma(const flo
   // while one block is multiplied out (a launch holds about one wave per
   // SIMD, so latency is hidden inside the wave)
   AttBlock<HD> bk[NB];
-  att_load<HD>(bk[0], pool, g, koff, voff, spg, c0, c1, c0, col, grp);   // first block in flight during the q set-up
+  if (live) att_load<HD>(bk[0], pool, g, koff, voff, spg, c0, c1, c0, col, grp);   // first block in flight during the q set-up
   // Q^T fragments (lanes >= rep: zero padding columns), parked in LDS in lane
   // order so that each lane reads back its own 16-byte pieces
-  __shared__ __attribute__((aligned(16))) u32x4_t sq[2][HD / 32][64];
+  __shared__ __attribute__((aligned(16))) u32x4_t sq_w[W][2][HD / 32][64];
+  auto& sq = sq_w[wave];
   {
     bf16x8_t qh[HD / 32], ql[HD / 32];
     att_load_q<HD>(q + ((int64_t)r * n_q + kvh * rep + min(col, rep - 1)) * HD, col < rep, grp, qh, ql);
@@ -448,6 +464,43 @@ __global__ __launch_bounds__(64, NB > 2 ? 1 : 2) void k_attention_mfma(const flo
       }
     }
     if (done) break;
+  }
+  if constexpr (W > 1) {
+    // Merge of the W chunk states, in chunk order.  Each wave parks its state
+    // in its own q area (free after its last block): output rows [col][HD]
+    // for its query heads, then (m, l) per head, m in log2 units.
+    float* so = reinterpret_cast<float*>(&sq[0][0][0]);
+    float* sml = so + ATT_MAX_REP * HD;
+    static_assert(ATT_MAX_REP * HD * 4 + ATT_MAX_REP * 8 <= 2 * (HD / 32) * 64 * 16, "state fits the q area");
+    if (col < rep) {
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) so[col * HD + dt * 16 + 4 * grp + e] = st.o[dt][e];
+      if (grp == 0) {
+        sml[2 * col] = st.m;
+        sml[2 * col + 1] = st.l;
+      }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < rep * HD; i += 64 * W) {
+      const int h = i / HD, d = i - h * HD;
+      float M = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < W; ++c)
+        M = fmaxf(M, reinterpret_cast<const float*>(&sq_w[c][0][0][0])[ATT_MAX_REP * HD + 2 * h]);
+      float L = 0.f, o = 0.f;
+#pragma unroll
+      for (int c = 0; c < W; ++c) {
+        const float* sc = reinterpret_cast<const float*>(&sq_w[c][0][0][0]);
+        const float mc = sc[ATT_MAX_REP * HD + 2 * h];
+        const float f = mc == -INFINITY ? 0.f : exp2f(mc - M);   // an empty chunk weighs 0
+        L += f * sc[ATT_MAX_REP * HD + 2 * h + 1];
+        o += f * sc[h * HD + d];
+      }
+      act_store<1>(out, ((int64_t)r * n_q + kvh * rep + h) * HD + d, o / L);
+    }
+    return;
   }
   if (col < rep) {
     if (plan.n_slots == 1) {   // the whole context in one work item: normalise and write the activation
@@ -813,18 +866,31 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
   if (dtype == 1) {
     // two 16-slot pages per 32-token block
     if (g.page_tok != 16) return hipErrorInvalidValue;
-    const int64_t nb = (int64_t)n_chunks * n_kv * rows_ub;
+    const int W = att_merges_in_kernel(dtype, plan, rows_ub, n_kv) ? n_chunks : 1;
+    const int64_t nb = (int64_t)(W == 1 ? n_chunks : 1) * n_kv * rows_ub;
     const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
-#define RG_ATT_MFMA(HD)                                                                                          \
-    att_launch(k_attention_mfma<HD, 2>, grid1, dim3(64), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer,     \
+#define RG_ATT_W(HD, WV)                                                                                          \
+    att_launch(k_attention_mfma<HD, 2, WV>, grid1, dim3(64 * WV), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
                page_tab, tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, ActOut{out, a_plane}, \
                d_rows)
+#define RG_ATT_MFMA(HD)                                                                                          \
+    switch (W) {                                                                                                 \
+      case 1: RG_ATT_W(HD, 1); break;                                                                            \
+      case 2: RG_ATT_W(HD, 2); break;                                                                            \
+      case 3: RG_ATT_W(HD, 3); break;                                                                            \
+      case 4: RG_ATT_W(HD, 4); break;                                                                            \
+      case 5: RG_ATT_W(HD, 5); break;                                                                            \
+      case 6: RG_ATT_W(HD, 6); break;                                                                            \
+      case 7: RG_ATT_W(HD, 7); break;                                                                            \
+      default: RG_ATT_W(HD, 8); break;                                                                           \
+    }
     switch (head_dim) {
       case 64: RG_ATT_MFMA(64); break;
       case 128: RG_ATT_MFMA(128); break;
       default: return hipErrorInvalidValue;
     }
 #undef RG_ATT_MFMA
+#undef RG_ATT_W
   } else
     att_launch(k_attention<float>, grid, dim3(256), st, q, n_q, n_kv, head_dim, (const float*)kv_pool, g, layer,
                page_tab, tab_stride, row_tab, row_pos, row_beg, plan, part_o, part_ml, d_rows);

@@ -112,6 +112,16 @@ struct AttPlan {
   int n_slots;     // pre_slots + n_chunks
 };
 
+// bf16 models whose rows take 2..8 context chunks (and no prefix pass) run one
+// workgroup per (row, kv head) whose waves merge the chunks themselves:
+// launch_attention then writes the activation and no merge launch follows.
+// Only where rows_ub * n_kv gives every CU a workgroup: with fewer, the
+// per-chunk grid plus a merge launch keeps more CUs busy and is faster.
+inline bool att_merges_in_kernel(int dtype, const AttPlan& plan, int rows_ub, int n_kv) {
+  return dtype == 1 && plan.pre_slots == 0 && plan.n_chunks >= 2 && plan.n_chunks <= 8 &&
+         (int64_t)rows_ub * n_kv >= 256;
+}
+
 // Per-row pass.  Row r covers positions row_beg[r]..row_pos[r] of page table
 // row_tab[r] (at most max_ctx tokens), cut into n_chunks equal chunks
 // (rounded up to 32 tokens); each (row, kv head, chunk) work item writes a
