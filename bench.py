@@ -212,6 +212,86 @@ def eb_sweep(args):
                       "steps_per_arm": T, "effective_batch": EB, "sizes": list(sizes), "arms": arms}), flush=True)
 
 
+def rows_sweep(args):
+    """Decode-step time at fixed small batches: rollouts of N = 16, 32, 64 and
+    128 sequences (groups of 16 on the workload's first prompts), every
+    completion forced to L tokens, so every decode step runs at N rows with
+    contexts from the prompt length to prompt length + L.  Best of two timed
+    rollouts after one untimed one; the decode time is the library's own
+    device-timeline phase.  Prints one JSON line."""
+    import torch
+    import paper_2606_02218_amd as rg
+    from workload import get_config, make_weights, make_inputs
+
+    L = args.rows_sweep
+    wl = get_config(args.workload)
+    shape = wl.shape
+    inp = make_inputs(wl, 0)
+    G, sizes = 16, (16, 32, 64, 128)
+    P_max = max(sizes) // G
+    if P_max > wl.n_prompts:
+        raise SystemExit(f"--rows-sweep needs {P_max} prompts; {wl.name} has {wl.n_prompts}")
+    pol = rg.Policy(shape, make_weights(shape, 0), max_seqs=max(sizes), max_prompts=P_max,
+                    max_prompt_tokens=P_max * wl.prompt_len, max_context=wl.prompt_len + L)
+    dev = torch.device("cuda")
+    res = {}
+    for N in sizes:
+        P = N // G
+        prompts = torch.from_numpy(inp.prompts[:P]).to(dev)
+        fl = np.full(N, L, dtype=np.int32)
+        out = (torch.empty((N, L), dtype=torch.int32, device=dev), torch.empty(N, dtype=torch.int32, device=dev),
+               torch.empty((N, L), dtype=torch.float32, device=dev))
+        pol.rollout(prompts, [G] * P, L, 7, forced_len=fl, out=out)
+        best = None
+        for r in range(2):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pol.rollout(prompts, [G] * P, L, 8 + r, forced_len=fl, out=out)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            pf, dc = pol.phase_times()
+            if best is None or dc < best[2]:
+                best = (wall, pf, dc)
+        wall, pf, dc = best
+        res[str(N)] = {"decode_ms": round(dc, 1), "ms_per_step": round(dc / (L - 1), 4), "prefill_ms": round(pf, 2),
+                       "wall_s": round(wall, 3)}
+        print(f"# {N} rows: {dc / (L - 1):.3f} ms per decode step", file=sys.stderr, flush=True)
+    print(json.dumps({"rows_sweep": wl.name, "forced_len": L, "decode_steps": L - 1, "prompt_len": wl.prompt_len,
+                      "rows": res}), flush=True)
+
+
+def launch_floor(n_kernels):
+    """Replay cost per kernel of a captured graph of n_kernels dependent tiny
+    elementwise kernels (torch's in-place add on 256 floats): the floor that a
+    decode step's own kernels sit above.  Prints one JSON line."""
+    import torch
+    x = torch.zeros(256, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            x.add_(1.0)
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(n_kernels):
+            x.add_(1.0)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    R = 50
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(R):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / R
+    expect = float(3 + (3 + R) * n_kernels)
+    print(json.dumps({"launch_floor_kernels": n_kernels, "us_per_replay": round(us, 1),
+                      "us_per_kernel": round(us / n_kernels, 3), "check": float(x[0].item()) == expect}), flush=True)
+
+
 def loss_forward_flops(shape, G, plen, lengths):
     """Algorithmic flops (one bf16 product per multiply-add pair) of the
     teacher-forced completion rows, per kernel class: R = sum(L - 1) rows
@@ -450,6 +530,10 @@ def main():
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the HBM copy / read and bf16 GEMM ceilings and exit")
+    ap.add_argument("--rows-sweep", type=int, default=0, metavar="L",
+                    help="only time decode steps at 16, 32, 64 and 128 rows (completions forced to L tokens) and exit")
+    ap.add_argument("--launch-floor", type=int, default=0, metavar="N",
+                    help="only time the replay of a graph of N tiny dependent kernels and exit")
     ap.add_argument("--prefill-probe", type=int, default=0, metavar="K",
                     help="only run K rollouts of the workload's prompts with every completion forced to 2 tokens "
                          "(the prefill and one full-batch decode step; a short command for counter passes) and exit")
@@ -472,6 +556,12 @@ def main():
         return
     if args.eb_sweep:
         eb_sweep(args)
+        return
+    if args.rows_sweep:
+        rows_sweep(args)
+        return
+    if args.launch_floor:
+        launch_floor(args.launch_floor)
         return
     if args.loss_forward:
         loss_forward(args)
