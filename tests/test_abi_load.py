@@ -140,12 +140,17 @@ def test_missing_library_fails_loudly(monkeypatch):
 @pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
 def test_decode_attention_chunk_plan():
     """The chunk plan a decode step's attention takes (host logic, no GPU):
-    the multi-chunk GPU test's rollout and the 1.5B workload below 257 rows
-    cut every row's context into several chunks."""
+    the multi-chunk GPU test's rollout and the 1.5B workload at every row
+    count cut each row's context into several chunks; from 512 to 2048
+    (row, kv head) pairs two, merged inside the kernel; beyond that, or for
+    contexts under 512 tokens, one."""
     import paper_2606_02218_amd as rg
     assert rg.decode_attention_chunks(5, 2, 2300 + 10) >= 3
     for rows in (1, 16, 64, 128, 256):
         assert rg.decode_attention_chunks(rows, 2, 512 + 4096) >= 2, rows
-    assert rg.decode_attention_chunks(512, 2, 512 + 4096) == 1
+    for rows in (384, 512, 1024):
+        assert rg.decode_attention_chunks(rows, 2, 512 + 4096) == 2, rows
+    assert rg.decode_attention_chunks(2048, 2, 512 + 4096) == 1
+    assert rg.decode_attention_chunks(512, 2, 400) == 1
     with pytest.raises(rg.RolloutError):
         rg.decode_attention_chunks(0, 2, 100)
