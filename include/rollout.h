@@ -340,10 +340,12 @@ int rg_phase_times(const rg_policy* pol, double* prefill_ms, double* decode_ms);
  * sequences (rounded up to the step's row bucket: 16, 32, 64, 128, 256, 384,
  * then multiples of 256), `n_kv` kv heads and the rollout's longest context
  * `ctx_max` (longest prompt + max_new).  Every row's context is cut into that
- * many chunks of at least 128 tokens (fewer when the context is shorter), each
- * chunk's partial softmax is written out and a merge kernel combines them
- * (more than one chunk).  A test and measurement aid; RG_EINVAL (< 0) for a
- * non-positive argument. */
+ * many chunks of at least 128 tokens (fewer when the context is shorter).  For
+ * bf16 models with 2 to 8 chunks and at least 256 (row, kv head) pairs, one
+ * workgroup per pair combines its chunks' partial softmax results in LDS;
+ * otherwise (more than one chunk) each chunk's partial is written out and a
+ * merge kernel combines them.  A test and measurement aid; RG_EINVAL (< 0)
+ * for a non-positive argument. */
 int32_t rg_decode_attention_chunks(int32_t rows, int32_t n_kv, int32_t ctx_max);
 
 /* Kernel classes timed under RG_FLAG_PROFILE. */
