@@ -435,6 +435,78 @@ __global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restr
   }
 }
 
+// QKV epilogue of split partials for bf16 models, 16 bytes at a time: thread
+// u of row r owns packed columns c..c+3 (c = 32 (u / 4) + 4 (u % 4), in the
+// lower half of a 32-column group) and their rotation partners c+16..c+19.
+// The partials of both column quads are summed in split order (as split_sum),
+// rotated, and written as one 16-byte q piece per half or one 8-byte key piece
+// per half (values: their transposed layout, one element at a time).  Same
+// arithmetic as qkv_store; one wave per 64 quads of a row.
+__global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  constexpr int BATCH = 16;
+  const int r = blockIdx.y;
+  const int u = blockIdx.x * 64 + threadIdx.x;
+  if (r >= *d_rows || u >= N / 8) return;
+  const int c = (u >> 2) * 32 + (u & 3) * 4;
+  const int hd = ep.hd, half = hd / 2;
+  const int head = c / hd, p = c % hd, d = (p >> 5) * 16 + (p & 15);
+  const int pos = ep.row_pos[r];
+  const f4* pr = reinterpret_cast<const f4*>(ep.part + (int64_t)r * N + c);
+  const int64_t pst4 = ep.part_stride / 4;
+  f4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < S; s0 += BATCH) {
+    f4 ta[BATCH], tb[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      ta[j] = s0 + j < S ? pr[(s0 + j) * pst4] : f4{0.f, 0.f, 0.f, 0.f};
+      tb[j] = s0 + j < S ? pr[(s0 + j) * pst4 + 4] : f4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      a += ta[j];
+      b += tb[j];
+    }
+  }
+  bf16_t* pool = (bf16_t*)ep.kv_pool;
+  const int n_rot = ep.n_q + ep.n_kv;
+  if (head >= n_rot) {                               // value head: no rotation, V^T layout
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
+    bf16_t* vb = pool + (int64_t)page * ep.geom.page_stride + (int64_t)ep.layer * ep.geom.layer_stride +
+                 ((int64_t)ep.n_kv + head - n_rot) * 16 * hd;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vb[kv_v_off(pos & 15, d + e, hd)] = f32_to_bf16(a[e]);
+      vb[kv_v_off(pos & 15, d + e + half, hd)] = f32_to_bf16(b[e]);
+    }
+    return;
+  }
+  const f4 co = *reinterpret_cast<const f4*>(ep.rope_cos + (int64_t)pos * half + d);
+  const f4 si = *reinterpret_cast<const f4*>(ep.rope_sin + (int64_t)pos * half + d);
+  f4 ra, rb;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    ra[e] = a[e] * co[e] - b[e] * si[e];
+    rb[e] = b[e] * co[e] + a[e] * si[e];
+  }
+  if (head < ep.n_q) {
+    float* qo = ep.q_out + ((int64_t)r * ep.n_q + head) * hd;
+    *reinterpret_cast<f4*>(qo + d) = ra;
+    *reinterpret_cast<f4*>(qo + d + half) = rb;
+  } else {
+    const int page = ep.page_tab[(int64_t)ep.row_tab[r] * ep.tab_stride + pos / 16];
+    bf16_t* kp = pool + (int64_t)page * ep.geom.page_stride + (int64_t)ep.layer * ep.geom.layer_stride +
+                 (int64_t)(head - ep.n_q) * 16 * hd;
+    uint2 ka, kb;
+    ka.x = (uint32_t)f32_to_bf16(ra[0]) | ((uint32_t)f32_to_bf16(ra[1]) << 16);
+    ka.y = (uint32_t)f32_to_bf16(ra[2]) | ((uint32_t)f32_to_bf16(ra[3]) << 16);
+    kb.x = (uint32_t)f32_to_bf16(rb[0]) | ((uint32_t)f32_to_bf16(rb[1]) << 16);
+    kb.y = (uint32_t)f32_to_bf16(rb[2]) | ((uint32_t)f32_to_bf16(rb[3]) << 16);
+    *reinterpret_cast<uint2*>(kp + kv_k_off(pos & 15, d)) = ka;
+    *reinterpret_cast<uint2*>(kp + kv_k_off(pos & 15, d + half)) = kb;
+  }
+}
+
 // Sum of split partials + epilogue: one block of 128 threads per (128
 // columns, row).  SPLIT: activation output as hi/lo bf16 planes.
 template <int EPI, int SPLIT, typename KV>
@@ -519,6 +591,12 @@ hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, c
     else return hipErrorInvalidValue;   // rows wider than 8192
 #undef RG_SRN
     return hipGetLastError();
+  }
+  if constexpr (SPLIT == 1) {
+    if (ep.mode == GEMM_EPI_QKV && N % 32 == 0 && ep.hd % 32 == 0 && ep.part_stride % 4 == 0) {
+      hipLaunchKernelGGL(k_qkv_epilogue4, dim3((N / 8 + 63) / 64, rows_ub), dim3(64), 0, st, d_rows, N, S, ep);
+      return hipGetLastError();
+    }
   }
   dim3 grid((N + 127) / 128, rows_ub);
   switch (ep.mode) {
