@@ -240,7 +240,7 @@ void choose_splits(const rg_policy* pol, int N, int rows_ub, int K, int* splits,
     // partials are small), and only as far as the fp32 partials (written
     // once, read once: 8 bytes per output element and split) stay within
     // twice the weight bytes or 24 MiB.
-    const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub, N), bn = gemm_tile_cols(pol->dtype, rows_ub, N);
+    const int64_t bm = gemm_tile_rows(pol->dtype, rows_ub, N), bn = gemm_tile_cols(pol->dtype, rows_ub, N, K);
     const int64_t blocks = ceil_div(N, bn) * ceil_div(rows_ub, bm);
     const int64_t target = N >= 8192 ? RG_GEMM_TARGET : 2 * RG_GEMM_TARGET;
     if (blocks < RG_GEMM_FULL) S = (int)ceil_div(target, blocks);

@@ -632,13 +632,25 @@ int gemm_tile_rows(int dtype, int rows_ub, int N) {
 }
 
 // Tiles of 256 rows are 256 x 256 (64 x 128 per wave: twice the MFMA work per
-// LDS fragment, which only pays with many blocks); gate/up at 33-64 rows 64
-// columns; all others 128 columns.
-int gemm_tile_cols(int dtype, int rows_ub, int N) {
-  if (gemm_tile_rows(dtype, rows_ub, N) == 256) return 256;
-  // wide outputs (gate/up) at 33-64 rows: 32 x 64 tiles, twice the blocks
-  // of 32 x 128 (1.5B gate/up at 64 rows 23.0 -> 20.4 us a launch)
-  if (dtype == 1 && rows_ub > 32 && rows_ub <= 64 && N >= 8192) return 64;
+// LDS fragment, which only pays with many blocks).  32-row tiles take 64
+// columns where that measured faster in the rollout (1.5B group step, ms per
+// bucket): wide outputs (gate/up) at 33-64 rows, which doubles their blocks
+// (644 -> 571 ms); narrow outputs at 17-64 rows, and at 65-128 rows those
+// with K <= 2N (QKV, O), where the same block count then needs half the
+// split-K factor and the split reduction reads half the partials (64 rows:
+// QKV + O + down 1096 -> 993 ms; 128 rows: QKV + O 702 -> 643 ms); and the
+// unsplit QKV (N > K) at 512 rows and more (512 -> 471 ms).  All others
+// 128 columns.  A tile shape that changes the split factor changes where the
+// fp32 split sums are cut, so results move within fp32 rounding.
+int gemm_tile_cols(int dtype, int rows_ub, int N, int K) {
+  const int bm = gemm_tile_rows(dtype, rows_ub, N);
+  if (bm == 256) return 256;
+  if (dtype == 1 && bm == 32) {
+    if (N >= 8192) return rows_ub > 32 && rows_ub <= 64 ? 64 : 128;
+    if (rows_ub <= 64) return 64;
+    if (rows_ub <= 128 && K <= 2 * N) return 64;
+    if (rows_ub >= 512 && N > K) return 64;
+  }
   return 128;
 }
 
@@ -655,7 +667,7 @@ hipError_t launch_gemm(int dtype, const void* A, int lda, int64_t a_plane, const
     switch (gemm_tile_rows(dtype, rows_ub, N)) {
       case 16: e = launch_tiled<16, 128, 1, 2, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st); break;
       case 32:
-        if (gemm_tile_cols(dtype, rows_ub, N) == 64)
+        if (gemm_tile_cols(dtype, rows_ub, N, K) == 64)
           e = launch_tiled<32, 64, 1, 2, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st);
         else
           e = launch_tiled<32, 128, 1, 4, 1>(A, lda, a_plane, W, ldw, d_rows, rows_ub, N, K, splits, k_per_split, ep, st);

@@ -47,7 +47,7 @@ bool rg_launch_events_armed();
 
 // Output tile rows / columns launch_gemm uses for a row bound and width N.
 int gemm_tile_rows(int dtype, int rows_ub, int N);
-int gemm_tile_cols(int dtype, int rows_ub, int N);
+int gemm_tile_cols(int dtype, int rows_ub, int N, int K);
 
 // Largest split-K factor of a projection.
 constexpr int GEMM_MAX_SPLITS = 32;
