@@ -633,22 +633,32 @@ int gemm_tile_rows(int dtype, int rows_ub, int N) {
 
 // Tiles of 256 rows are 256 x 256 (64 x 128 per wave: twice the MFMA work per
 // LDS fragment, which only pays with many blocks).  32-row tiles take 64
-// columns where that measured faster in the rollout (1.5B group step, ms per
-// bucket): wide outputs (gate/up) at 33-64 rows, which doubles their blocks
-// (644 -> 571 ms); narrow outputs at 17-64 rows, and at 65-128 rows those
-// with K <= 2N (QKV, O), where the same block count then needs half the
-// split-K factor and the split reduction reads half the partials (64 rows:
-// QKV + O + down 1096 -> 993 ms; 128 rows: QKV + O 702 -> 643 ms); and the
-// unsplit QKV (N > K) at 512 rows and more (512 -> 471 ms).  All others
-// 128 columns.  A tile shape that changes the split factor changes where the
-// fp32 split sums are cut, so results move within fp32 rounding.
+// columns where that measured faster in the rollout (1.5B and 7B group steps,
+// ms per row bucket):
+// * wide outputs (gate/up) at 33-64 rows when 128-column tiles leave fewer
+//   than two blocks per CU (1.5B: 280 blocks -> 560, 644 -> 571 ms; 7B's
+//   592 blocks measured slower at 1,184);
+// * narrow outputs at 17-64 rows, and at 65-128 rows those with K <= 2N (QKV,
+//   O), while the 64-column tiles still number fewer than the engine's
+//   no-split threshold: the same block count then needs half the split-K
+//   factor and the split reduction reads half the partials (1.5B at 64 rows:
+//   QKV + O + down 1096 -> 993 ms; at 128 rows QKV + O 702 -> 643 ms).  7B's
+//   QKV at 128 rows would cross the threshold and run unsplit, 1.6x slower;
+// * the unsplit QKV (N > K) at 512 rows and more (1.5B: 512 -> 471 ms).
+// All others 128 columns.  A tile shape that changes the split factor
+// changes where the fp32 split sums are cut, so results move within fp32
+// rounding.
 int gemm_tile_cols(int dtype, int rows_ub, int N, int K) {
   const int bm = gemm_tile_rows(dtype, rows_ub, N);
   if (bm == 256) return 256;
   if (dtype == 1 && bm == 32) {
-    if (N >= 8192) return rows_ub > 32 && rows_ub <= 64 ? 64 : 128;
-    if (rows_ub <= 64) return 64;
-    if (rows_ub <= 128 && K <= 2 * N) return 64;
+    constexpr int64_t kNoSplitBlocks = 256;   // the engine splits K below this many output tiles
+    const int64_t row_tiles = (rows_ub + 31) / 32;
+    if (N >= 8192)
+      return rows_ub > 32 && rows_ub <= 64 && (int64_t)((N + 127) / 128) * row_tiles < 2 * kNoSplitBlocks ? 64 : 128;
+    const bool splits64 = (int64_t)((N + 63) / 64) * row_tiles < kNoSplitBlocks;
+    if (rows_ub <= 64 && splits64) return 64;
+    if (rows_ub <= 128 && K <= 2 * N && splits64) return 64;
     if (rows_ub >= 512 && N > K) return 64;
   }
   return 128;
