@@ -45,17 +45,20 @@ __device__ __forceinline__ void kv_store(KV* p, float v);
 template <> __device__ __forceinline__ void kv_store<float>(float* p, float v) { *p = v; }
 template <> __device__ __forceinline__ void kv_store<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
 
-// Sum of the split partials of element (r, c), in split order.  All loads
-// (at most GEMM_MAX_SPLITS) are issued before the first add.
+// Sum of the split partials of element (r, c), in split order.  The loads
+// of a batch of 16 splits are all issued before its first add.
 __device__ __forceinline__ float split_sum(const GemmEpi& ep, int S, int64_t off) {
+  constexpr int BATCH = 16;
   const float* p = ep.part + off;
   const int64_t st = ep.part_stride;
-  float v[GEMM_MAX_SPLITS];
-#pragma unroll
-  for (int s = 0; s < GEMM_MAX_SPLITS; ++s) v[s] = s < S ? p[s * st] : 0.f;
   float acc = 0.f;
+  for (int s0 = 0; s0 < S; s0 += BATCH) {
+    float v[BATCH];
 #pragma unroll
-  for (int s = 0; s < GEMM_MAX_SPLITS; ++s) acc += v[s];
+    for (int j = 0; j < BATCH; ++j) v[j] = s0 + j < S ? p[(s0 + j) * st] : 0.f;
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) acc += v[j];
+  }
   return acc;
 }
 
@@ -166,15 +169,19 @@ __device__ __forceinline__ void qkv_tile_store(const f32x4_t (&acc)[WM][WN], con
 }
 
 // Epilogue of a finished tile whose split partials are in ep.part: rows
-// m0..m0+BM-1 (< M), columns n0..n0+BN-1 (< N).  Every thread of the block
-// calls it.
+// m0..m0+BM-1, columns n0..n0+BN-1 (< N); only rows below M are stored.
+// STORE, RESIDUAL and SWIGLU sum the partials of every row of the tile (all
+// inside the partial buffer) before testing it against M, so their loads do
+// not wait for the row count; QKV needs the row's position and page and
+// tests first.  Every thread of the block calls it.
 template <int EPI, int BM, int BN, int NT, int SPLIT, typename KV>
 __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, int N, int tid) {
   if constexpr (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_RESIDUAL) {
     for (int i = tid; i < BM * BN; i += NT) {
       const int r = m0 + i / BN, c = n0 + i % BN;
-      if (r >= M || c >= N) continue;
+      if (c >= N) continue;
       const float v = split_sum(ep, S, (int64_t)r * N + c);
+      if (r >= M) continue;
       if constexpr (EPI == GEMM_EPI_STORE) ep.C[(int64_t)r * ep.ldc + c] = v;
       else ep.x[(int64_t)r * ep.ldx + c] += v;
     }
@@ -182,9 +189,10 @@ __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, i
     for (int i = tid; i < BM * (BN / 2); i += NT) {
       const int r = m0 + i / (BN / 2), q = i % (BN / 2);
       const int gc = n0 + (q >> 4) * 32 + (q & 15);    // gate column; up is 16 further
-      if (r >= M || gc >= N) continue;
+      if (gc >= N) continue;
       const float gt = split_sum(ep, S, (int64_t)r * N + gc);
       const float up = split_sum(ep, S, (int64_t)r * N + gc + 16);
+      if (r >= M) continue;
       act_store<SPLIT>(ep.act, (int64_t)r * ep.act_ld + (gc >> 5) * 16 + (q & 15), gt / (1.0f + expf(-gt)) * up);
     }
   } else {  // GEMM_EPI_QKV: packed columns; a lower-half tile owns the rotated pair
@@ -212,7 +220,14 @@ __device__ __forceinline__ u32x4_t load_w(const bf16_t* p) {
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
-    const int* __restrict__ d_rows, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy, int order1d) {
+    const int* __restrict__ d_rows, int rows_cap, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy,
+    int order1d) {
+  // The row count is read first but waited for only after the first K
+  // step's loads are issued: those clamp A rows to the launch's row bound
+  // rows_cap (>= the count; the activation buffer holds that many rows), so
+  // they do not depend on it.  Rows past the count are multiplied, never
+  // stored.
+  const int rows_now = *d_rows;
   constexpr int WAVES_M = BM / (16 * WM), WAVES_N = BN / (16 * WN);
   constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int LROW = BK + LDS_PAD;                // LDS row stride (elements)
@@ -246,9 +261,8 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
     ty = r0 + wi % rows_g;
     tx = wi / rows_g;
   }
-  const int M = *d_rows;
   const int m0 = ty * BM;
-  if (m0 >= M) return;
+  if (m0 >= rows_cap) return;
   const int n0 = tx * BN;
   const int kb0 = tz * k_per_split;
   const int ke = min(K, kb0 + k_per_split);
@@ -265,7 +279,7 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   _Pragma("unroll") for (int i = 0; i < A_PER_T; ++i) {                                                       \
     const int p = tid + i * NT;                                                                               \
     const int plane = p / A_PIECES, q = p % A_PIECES;                                                         \
-    const int row = min(m0 + q / (BK / 8), M - 1); /* rows past M are computed, never stored */              \
+    const int row = min(m0 + q / (BK / 8), rows_cap - 1); /* rows past M are computed, never stored */       \
     ra[S][i] = *reinterpret_cast<const u32x4_t*>(A + plane * a_plane + (int64_t)row * lda + (KK) + (q % (BK / 8)) * 8); \
   }                                                                                                           \
   _Pragma("unroll") for (int i = 0; i < W_PER_T; ++i) {                                                       \
@@ -293,6 +307,10 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
 #pragma unroll
   for (int s = 0; s < STAGES; ++s)
     if (kb0 + s * BK < ke) { RG_FETCH(s, kb0 + s * BK) }
+  // keeps the loads above in front of the row-count test (no sinking past it)
+  __asm__ volatile("" ::: "memory");
+  const int M = min(rows_now, rows_cap);
+  if (m0 >= M) return;
   for (int k = kb0; k < ke; k += STAGES * BK) {
 #pragma unroll
     for (int s = 0; s < STAGES; ++s) {
@@ -390,7 +408,10 @@ __global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restr
   constexpr int NT = 1024;
   constexpr int BATCH = CPT <= 2 ? 16 : 32 / CPT;   // splits loaded per batch
   const int r = blockIdx.x;
-  if (r >= *d_rows) return;
+  // Blocks of rows past the count (r < the launch's row bound, inside every
+  // buffer) run the same loads and sums but store nothing, so no load waits
+  // for the count.
+  const int rows_now = *d_rows;
   __shared__ float red[16];
   float* xr = ep.x + (int64_t)r * ep.ldx;
   const float* pr = ep.part + (int64_t)r * N;
@@ -428,7 +449,7 @@ __global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restr
 #pragma unroll
   for (int k = 0; k < CPT; ++k) {
     const int c = threadIdx.x + k * NT;
-    if (c < N) {
+    if (c < N && r < rows_now) {
       xr[c] = xv[k];
       act_store<SPLIT>(ep.norm_out, (int64_t)r * N + c, xv[k] * inv * gv[k]);
     }
@@ -447,11 +468,11 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
   constexpr int BATCH = 16;
   const int r = blockIdx.y;
   const int u = blockIdx.x * 64 + threadIdx.x;
-  if (r >= *d_rows || u >= N / 8) return;
+  const int rows_now = *d_rows;   // waited for after the partials' loads
+  if (u >= N / 8) return;
   const int c = (u >> 2) * 32 + (u & 3) * 4;
   const int hd = ep.hd, half = hd / 2;
   const int head = c / hd, p = c % hd, d = (p >> 5) * 16 + (p & 15);
-  const int pos = ep.row_pos[r];
   const f4* pr = reinterpret_cast<const f4*>(ep.part + (int64_t)r * N + c);
   const int64_t pst4 = ep.part_stride / 4;
   f4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
@@ -468,6 +489,9 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
       b += tb[j];
     }
   }
+  // a row past the count has no position or page yet
+  if (r >= rows_now) return;
+  const int pos = ep.row_pos[r];
   bf16_t* pool = (bf16_t*)ep.kv_pool;
   const int n_rot = ep.n_q + ep.n_kv;
   if (head >= n_rot) {                               // value head: no rotation, V^T layout
@@ -512,8 +536,11 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
 template <int EPI, int SPLIT, typename KV>
 __global__ __launch_bounds__(128) void k_split_epilogue(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
   const int r = blockIdx.y;
-  if (r >= *d_rows) return;
-  tile_epilogue<EPI, 1, 128, 128, SPLIT, KV>(ep, S, r, blockIdx.x * 128, r + 1, N, threadIdx.x);
+  const int rows_now = *d_rows;
+  if constexpr (EPI == GEMM_EPI_QKV) {
+    if (r >= rows_now) return;
+  }
+  tile_epilogue<EPI, 1, 128, 128, SPLIT, KV>(ep, S, r, blockIdx.x * 128, rows_now, N, threadIdx.x);
 }
 
 // fp32 models: plain fp32 FMA, one thread per output, 64 columns x 4 rows per
@@ -559,10 +586,12 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
   do {                                                                                                        \
     if (ntw)                                                                                                  \
       hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, true>), grid, dim3(NT), 0, st,         \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep, gx, gy, order1d); \
+                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
+                         gx, gy, order1d);                                                                    \
     else                                                                                                      \
       hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, false>), grid, dim3(NT), 0, st,        \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, N, K, k_per_split, ep, gx, gy, order1d); \
+                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
+                         gx, gy, order1d);                                                                    \
   } while (0)
   if (splits > 1) {
     RG_TILED(GEMM_EPI_PARTIAL);
