@@ -70,9 +70,14 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
                                                    float* __restrict__ part_o, float* __restrict__ part_ml,
                                                    const int* __restrict__ d_rows) {
   const int r = blockIdx.z;
-  if (r >= *d_rows) return;
+  // the row's entries (r < the launch's row bound: inside the row arrays)
+  // are read alongside the row count and used only once r is below it
+  const int rows_now = *d_rows;
+  const int pos_r = row_pos[r], beg_r = row_beg[r], tab_r = row_tab[r];
+  __asm__ volatile("" ::: "memory");
+  if (r >= rows_now) return;
   const int kvh = blockIdx.y, chunk = blockIdx.x;
-  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
   const int c0 = beg + chunk * clen;
   if (c0 >= ctx) return;
@@ -89,7 +94,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
   for (int i = tid; i < rep * hd; i += blockDim.x)
     sq[i] = q[((int64_t)r * n_q + kvh * rep) * hd + i];
   if (tid < rep) { s_m[tid] = -INFINITY; s_l[tid] = 0.f; }
-  const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride;
+  const int32_t* tab = page_tab + (int64_t)tab_r * tab_stride;
   const int64_t koff = (int64_t)layer * g.layer_stride + (int64_t)kvh * 16 * hd;
   const int64_t voff = (int64_t)layer * g.layer_stride + ((int64_t)n_kv + kvh) * 16 * hd;
 
@@ -386,8 +391,13 @@ __global__ __launch_bounds__(64 * W, NB > 2 ? 1 : 2) void k_attention_mfma(const
     kvh = (int)(w % n_kv);
     r = (int)(w / n_kv);
   }
-  if (r >= *d_rows) return;                         // uniform over the workgroup
-  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  // the row's entries (r < rows_ub: inside the row arrays) are read
+  // alongside the row count and used only once r is below it
+  const int rows_now = *d_rows;
+  const int pos_r = row_pos[r], beg_r = row_beg[r], tab_r = row_tab[r];
+  __asm__ volatile("" ::: "memory");
+  if (r >= rows_now) return;                        // uniform over the workgroup
+  const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, n_chunks);
   const int c0 = beg + chunk * clen;                // a multiple of 16
   if constexpr (W == 1)
@@ -401,7 +411,7 @@ __global__ __launch_bounds__(64 * W, NB > 2 ? 1 : 2) void k_attention_mfma(const
   __shared__ int spg_w[W][ATT_MAX_CHUNK_PAGES];
   int* spg = spg_w[wave];
   {
-    const int32_t* tab = page_tab + (int64_t)row_tab[r] * tab_stride + (c0 >> 4);
+    const int32_t* tab = page_tab + (int64_t)tab_r * tab_stride + (c0 >> 4);
     const int npg = (c1 - c0 + 15) >> 4;
     for (int i = lane; i < npg; i += 64) spg[i] = tab[i];
     __syncthreads();
@@ -802,9 +812,12 @@ __global__ void k_attn_merge(const float* __restrict__ part_o, const float* __re
                              const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_beg,
                              AttPlan plan, ActOut out, const int* __restrict__ d_rows) {
   const int r = blockIdx.x;
-  if (r >= *d_rows) return;
+  const int rows_now = *d_rows;
+  const int pos_r = row_pos[r], beg_r = row_beg[r];   // r < the row bound: inside the row arrays
+  __asm__ volatile("" ::: "memory");
+  if (r >= rows_now) return;
   const int h = blockIdx.y;
-  const int ctx = row_pos[r] + 1, beg = row_beg[r];
+  const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
   const int npre = plan.pre_slots ? (beg + plan.pre_chunk - 1) / plan.pre_chunk : 0;   // prefix slots written
   const int nc = npre + (ctx - beg + clen - 1) / clen;                                  // slots holding context

@@ -171,17 +171,17 @@ __device__ __forceinline__ void qkv_tile_store(const f32x4_t (&acc)[WM][WN], con
 // Epilogue of a finished tile whose split partials are in ep.part: rows
 // m0..m0+BM-1, columns n0..n0+BN-1 (< N); only rows below M are stored.
 // STORE, RESIDUAL and SWIGLU sum the partials of every row of the tile (all
-// inside the partial buffer) before testing it against M, so their loads do
-// not wait for the row count; QKV needs the row's position and page and
+// inside the partial buffer; columns past N read a column in range) before
+// testing row and column, so their loads wait neither for the row count nor
+// for a test of a kernel argument; QKV needs the row's position and page and
 // tests first.  Every thread of the block calls it.
 template <int EPI, int BM, int BN, int NT, int SPLIT, typename KV>
 __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, int N, int tid) {
   if constexpr (EPI == GEMM_EPI_STORE || EPI == GEMM_EPI_RESIDUAL) {
     for (int i = tid; i < BM * BN; i += NT) {
       const int r = m0 + i / BN, c = n0 + i % BN;
-      if (c >= N) continue;
-      const float v = split_sum(ep, S, (int64_t)r * N + c);
-      if (r >= M) continue;
+      const float v = split_sum(ep, S, (int64_t)r * N + min(c, N - 1));
+      if (r >= M || c >= N) continue;
       if constexpr (EPI == GEMM_EPI_STORE) ep.C[(int64_t)r * ep.ldc + c] = v;
       else ep.x[(int64_t)r * ep.ldx + c] += v;
     }
@@ -189,10 +189,10 @@ __device__ void tile_epilogue(const GemmEpi& ep, int S, int m0, int n0, int M, i
     for (int i = tid; i < BM * (BN / 2); i += NT) {
       const int r = m0 + i / (BN / 2), q = i % (BN / 2);
       const int gc = n0 + (q >> 4) * 32 + (q & 15);    // gate column; up is 16 further
-      if (gc >= N) continue;
-      const float gt = split_sum(ep, S, (int64_t)r * N + gc);
-      const float up = split_sum(ep, S, (int64_t)r * N + gc + 16);
-      if (r >= M) continue;
+      const int gl = min(gc, N - 17);                    // gc itself while in range (N % 32 == 0)
+      const float gt = split_sum(ep, S, (int64_t)r * N + gl);
+      const float up = split_sum(ep, S, (int64_t)r * N + gl + 16);
+      if (r >= M || gc >= N) continue;
       act_store<SPLIT>(ep.act, (int64_t)r * ep.act_ld + (gc >> 5) * 16 + (q & 15), gt / (1.0f + expf(-gt)) * up);
     }
   } else {  // GEMM_EPI_QKV: packed columns; a lower-half tile owns the rotated pair
@@ -217,11 +217,10 @@ __device__ __forceinline__ u32x4_t load_w(const bf16_t* p) {
   else return *reinterpret_cast<const u32x4_t*>(p);
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW>
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW, bool XO>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
-    const int* __restrict__ d_rows, int rows_cap, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy,
-    int order1d) {
+    const int* __restrict__ d_rows, int rows_cap, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy) {
   // The row count is read first but waited for only after the first K
   // step's loads are issued: those clamp A rows to the launch's row bound
   // rows_cap (>= the count; the activation buffer holds that many rows), so
@@ -242,7 +241,7 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
   __shared__ __attribute__((aligned(16))) bf16_t sW[BN * LROW];
 
   int tx = blockIdx.x, ty = blockIdx.y, tz = blockIdx.z;
-  if (order1d) {
+  if constexpr (XO) {
     // A 1-D grid of a multiple of 8 blocks, dealt to the 8 XCDs in turn:
     // XCD x = b % 8 takes the contiguous tile range [x*per, (x+1)*per)
     // (split-major), walked in groups of TILE_GROUP row tiles.  Within a
@@ -261,8 +260,7 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
     ty = r0 + wi % rows_g;
     tx = wi / rows_g;
   }
-  const int m0 = ty * BM;
-  if (m0 >= rows_cap) return;
+  const int m0 = ty * BM;   // < rows_cap: the grid has ceil(rows_cap / BM) row tiles
   const int n0 = tx * BN;
   const int kb0 = tz * k_per_split;
   const int ke = min(K, kb0 + k_per_split);
@@ -469,8 +467,9 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
   const int r = blockIdx.y;
   const int u = blockIdx.x * 64 + threadIdx.x;
   const int rows_now = *d_rows;   // waited for after the partials' loads
-  if (u >= N / 8) return;
-  const int c = (u >> 2) * 32 + (u & 3) * 4;
+  __builtin_assume(S >= 1);
+  const int uc = min(u, N / 8 - 1);   // a quad in range: u's own test comes after the loads
+  const int c = (uc >> 2) * 32 + (uc & 3) * 4;
   const int hd = ep.hd, half = hd / 2;
   const int head = c / hd, p = c % hd, d = (p >> 5) * 16 + (p & 15);
   const f4* pr = reinterpret_cast<const f4*>(ep.part + (int64_t)r * N + c);
@@ -490,7 +489,7 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
     }
   }
   // a row past the count has no position or page yet
-  if (r >= rows_now) return;
+  if (r >= rows_now || u >= N / 8) return;
   const int pos = ep.row_pos[r];
   bf16_t* pool = (bf16_t*)ep.kv_pool;
   const int n_rot = ep.n_q + ep.n_kv;
@@ -582,16 +581,23 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
   // by the other row tiles' blocks through L2, and non-temporal loads there
   // measured 12 % slower over the 1.5B group step.
   const bool ntw = gy == 1;
+  // The tile order is a template parameter, so that no kernel argument
+  // decides a branch ahead of the first loads.  Below 256 x 256 tiles the
+  // grouped order needs 8 or more row tiles, so it never meets ntw.
+#define RG_TILED_K(E, NTV, XOV)                                                                               \
+  hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, NTV, XOV>), grid, dim3(NT), 0, st,           \
+                     (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
+                     gx, gy)
 #define RG_TILED(E)                                                                                           \
   do {                                                                                                        \
-    if (ntw)                                                                                                  \
-      hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, true>), grid, dim3(NT), 0, st,         \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
-                         gx, gy, order1d);                                                                    \
-    else                                                                                                      \
-      hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, false>), grid, dim3(NT), 0, st,        \
-                         (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
-                         gx, gy, order1d);                                                                    \
+    if constexpr (BM == 256) {                                                                                \
+      if (ntw) RG_TILED_K(E, true, true);                                                                     \
+      else RG_TILED_K(E, false, true);                                                                        \
+    } else {                                                                                                  \
+      if (order1d) RG_TILED_K(E, false, true);                                                                \
+      else if (ntw) RG_TILED_K(E, true, false);                                                               \
+      else RG_TILED_K(E, false, false);                                                                       \
+    }                                                                                                         \
   } while (0)
   if (splits > 1) {
     RG_TILED(GEMM_EPI_PARTIAL);
@@ -605,6 +611,7 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
     }
   }
 #undef RG_TILED
+#undef RG_TILED_K
   return hipGetLastError();
 }
 
