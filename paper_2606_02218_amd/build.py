@@ -33,6 +33,9 @@ def _compile(src: str) -> str:
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,
            # compile all device code without packed fp32 instructions
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # the first 14 dwords of every kernel's arguments arrive in scalar
+           # registers at dispatch instead of through a load from memory
+           "-mllvm", "-amdgpu-kernarg-preload-count=14",
            "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd.insert(1, "-x")

@@ -74,8 +74,7 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ q, 
   // are read alongside the row count and used only once r is below it
   const int rows_now = *d_rows;
   const int pos_r = row_pos[r], beg_r = row_beg[r], tab_r = row_tab[r];
-  __asm__ volatile("" ::: "memory");
-  if (r >= rows_now) return;
+  if ((r >= rows_now) | ((pos_r | beg_r | tab_r) < 0)) return;   // entries of live rows are >= 0
   const int kvh = blockIdx.y, chunk = blockIdx.x;
   const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
@@ -359,44 +358,43 @@ __device__ __forceinline__ void att_load(AttBlock<HD>& b, const bf16_t* __restri
 // chunk c of the row's W chunks; at the end the waves merge their (max, sum,
 // output) states through LDS in chunk order and write the normalised
 // activation, so no merge kernel runs.
+// The arguments that locate a work item's row come first (14 dwords, which
+// the build preloads into scalar registers at dispatch): the row count and
+// the row's entries are then read without a load of the arguments first.
 template <int HD, int NB, int W>
-__global__ __launch_bounds__(64 * W, NB > 2 ? 1 : 2) void k_attention_mfma(const float* __restrict__ q, int n_q, int n_kv,
-                                                       const bf16_t* __restrict__ pool, KvGeom g, int layer,
-                                                       const int32_t* __restrict__ page_tab, int tab_stride,
-                                                       const int32_t* __restrict__ row_tab,
-                                                       const int32_t* __restrict__ row_pos,
-                                                       const int32_t* __restrict__ row_beg, AttPlan plan,
-                                                       int rows_ub, float* __restrict__ part_o,
-                                                       float* __restrict__ part_ml, ActOut out,
-                                                       const int* __restrict__ d_rows) {
+__global__ __launch_bounds__(64 * W, NB > 2 ? 1 : 2) void k_attention_mfma(
+    const int* __restrict__ d_rows, const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_beg,
+    const int32_t* __restrict__ row_tab, int n_chunks, int n_kv, int rows_ub, int n_q, int per_xcd,
+    const float* __restrict__ q, const int32_t* __restrict__ page_tab, int tab_stride, const bf16_t* __restrict__ pool,
+    KvGeom g, int layer, AttPlan plan, float* __restrict__ part_o, float* __restrict__ part_ml, ActOut out) {
   static_assert(HD % 32 == 0 && HD <= 256, "head_dim");
-  // XCD-aware order: the 1-D grid has a multiple of 8 blocks and blocks are
+  // XCD-aware order: the 1-D grid has 8 * per_xcd blocks and blocks are
   // dealt to the 8 XCDs round-robin, so XCD x = b % 8 takes the contiguous
   // work range [x*per_xcd, (x+1)*per_xcd): neighbouring rows (siblings of one
-  // prompt) share an XCD, whose L2 then holds their shared prefix.
-  const int n_chunks = plan.n_chunks;
-  const int64_t b = blockIdx.x;
-  const int64_t per_xcd = (int64_t)gridDim.x / 8;
-  const int64_t w = (b % 8) * per_xcd + b / 8;
+  // prompt) share an XCD, whose L2 then holds their shared prefix.  The
+  // launch keeps every index below 2^31.
+  const int b = (int)blockIdx.x;
+  const int w = (b % 8) * per_xcd + b / 8;
   const int wave = W == 1 ? 0 : (int)(threadIdx.x >> 6);
   int chunk, kvh, r;
   if constexpr (W == 1) {
-    if (w >= (int64_t)n_chunks * n_kv * rows_ub) return;
-    chunk = (int)(w % n_chunks);
-    kvh = (int)((w / n_chunks) % n_kv);
-    r = (int)(w / ((int64_t)n_chunks * n_kv));
+    if (w >= n_chunks * n_kv * rows_ub) return;
+    chunk = w % n_chunks;
+    kvh = (w / n_chunks) % n_kv;
+    r = w / (n_chunks * n_kv);
   } else {   // the workgroup's (row, kv head); n_chunks == W
-    if (w >= (int64_t)n_kv * rows_ub) return;
+    if (w >= n_kv * rows_ub) return;
     chunk = wave;
-    kvh = (int)(w % n_kv);
-    r = (int)(w / n_kv);
+    kvh = w % n_kv;
+    r = w / n_kv;
   }
-  // the row's entries (r < rows_ub: inside the row arrays) are read
-  // alongside the row count and used only once r is below it
+  // The row's entries (r < rows_ub: inside the row arrays) are read
+  // alongside the row count and used only once r is below it.  Rows below
+  // the count hold entries >= 0, so the sign test only joins their loads to
+  // the row test's one wait (the compiler would otherwise sink them past it).
   const int rows_now = *d_rows;
   const int pos_r = row_pos[r], beg_r = row_beg[r], tab_r = row_tab[r];
-  __asm__ volatile("" ::: "memory");
-  if (r >= rows_now) return;                        // uniform over the workgroup
+  if ((r >= rows_now) | ((pos_r | beg_r | tab_r) < 0)) return;   // uniform over the workgroup
   const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, n_chunks);
   const int c0 = beg + chunk * clen;                // a multiple of 16
@@ -808,14 +806,13 @@ __global__ __launch_bounds__(64 * ATT_TILE_MAX_WAVES) void k_attention_tile(
 }
 
 template <int SPLIT>
-__global__ void k_attn_merge(const float* __restrict__ part_o, const float* __restrict__ part_ml, int n_q, int hd,
-                             const int32_t* __restrict__ row_pos, const int32_t* __restrict__ row_beg,
-                             AttPlan plan, ActOut out, const int* __restrict__ d_rows) {
+__global__ void k_attn_merge(const int* __restrict__ d_rows, const int32_t* __restrict__ row_pos,
+                             const int32_t* __restrict__ row_beg, const float* __restrict__ part_o,
+                             const float* __restrict__ part_ml, int n_q, int hd, AttPlan plan, ActOut out) {
   const int r = blockIdx.x;
   const int rows_now = *d_rows;
   const int pos_r = row_pos[r], beg_r = row_beg[r];   // r < the row bound: inside the row arrays
-  __asm__ volatile("" ::: "memory");
-  if (r >= rows_now) return;
+  if ((r >= rows_now) | ((pos_r | beg_r) < 0)) return;   // entries of live rows are >= 0
   const int h = blockIdx.y;
   const int ctx = pos_r + 1, beg = beg_r;
   const int clen = att_chunk_len(ctx - beg, plan.n_chunks);
@@ -881,11 +878,13 @@ hipError_t launch_attention(int dtype, const float* q, int n_q, int n_kv, int he
     if (g.page_tok != 16) return hipErrorInvalidValue;
     const int W = att_merges_in_kernel(dtype, plan, rows_ub, n_kv) ? n_chunks : 1;
     const int64_t nb = (int64_t)(W == 1 ? n_chunks : 1) * n_kv * rows_ub;
-    const dim3 grid1((unsigned)((nb + 7) / 8 * 8));
+    if (nb > INT32_MAX - 8) return hipErrorInvalidValue;
+    const int per_xcd = (int)((nb + 7) / 8);
+    const dim3 grid1((unsigned)(8 * per_xcd));
 #define RG_ATT_W(HD, WV)                                                                                          \
-    att_launch(k_attention_mfma<HD, 2, WV>, grid1, dim3(64 * WV), st, q, n_q, n_kv, (const bf16_t*)kv_pool, g, layer, \
-               page_tab, tab_stride, row_tab, row_pos, row_beg, plan, rows_ub, part_o, part_ml, ActOut{out, a_plane}, \
-               d_rows)
+    att_launch(k_attention_mfma<HD, 2, WV>, grid1, dim3(64 * WV), st, d_rows, row_pos, row_beg, row_tab, n_chunks, \
+               n_kv, rows_ub, n_q, per_xcd, q, page_tab, tab_stride, (const bf16_t*)kv_pool, g, layer, plan, part_o, \
+               part_ml, ActOut{out, a_plane})
 #define RG_ATT_MFMA(HD)                                                                                          \
     switch (W) {                                                                                                 \
       case 1: RG_ATT_W(HD, 1); break;                                                                            \
@@ -947,11 +946,11 @@ hipError_t launch_attn_merge(int dtype, const float* part_o, const float* part_m
   int threads = head_dim >= 64 ? 64 * ((head_dim + 63) / 64) : 64;
   const ActOut o{out, a_plane};
   if (dtype == 1)
-    hipLaunchKernelGGL(k_attn_merge<1>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos, row_beg,
-                       plan, o, d_rows);
+    hipLaunchKernelGGL(k_attn_merge<1>, grid, dim3(threads), 0, st, d_rows, row_pos, row_beg, part_o, part_ml, n_q,
+                       head_dim, plan, o);
   else
-    hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, part_o, part_ml, n_q, head_dim, row_pos, row_beg,
-                       plan, o, d_rows);
+    hipLaunchKernelGGL(k_attn_merge<0>, grid, dim3(threads), 0, st, d_rows, row_pos, row_beg, part_o, part_ml, n_q,
+                       head_dim, plan, o);
   return hipGetLastError();
 }
 

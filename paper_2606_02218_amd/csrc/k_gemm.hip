@@ -219,8 +219,10 @@ __device__ __forceinline__ u32x4_t load_w(const bf16_t* p) {
 
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW, bool XO>
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
-    const bf16_t* __restrict__ A, int lda, int64_t a_plane, const bf16_t* __restrict__ W, int ldw,
-    const int* __restrict__ d_rows, int rows_cap, int N, int K, int k_per_split, GemmEpi ep, int gx, int gy) {
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, const int* __restrict__ d_rows, int64_t a_plane,
+    int lda, int ldw, int rows_cap, int N, int K, int k_per_split, int gx, int gy, GemmEpi ep) {
+  // (the arguments the first loads need come first: 14 dwords, which the
+  // build preloads into scalar registers at dispatch)
   // The row count is read first but waited for only after the first K
   // step's loads are issued: those clamp A rows to the launch's row bound
   // rows_cap (>= the count; the activation buffer holds that many rows), so
@@ -402,7 +404,10 @@ __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_ge
 // and the row stays in registers between the sum of squares and the store.
 // The sums run in split order, as in split_sum.
 template <int SPLIT, int CPT>
-__global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+__global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restrict__ d_rows,
+                                                               const float* __restrict__ part, int64_t pst,
+                                                               float* __restrict__ x, const float* __restrict__ norm_g,
+                                                               int N, int S, int ldx, GemmEpi ep) {
   constexpr int NT = 1024;
   constexpr int BATCH = CPT <= 2 ? 16 : 32 / CPT;   // splits loaded per batch
   const int r = blockIdx.x;
@@ -411,15 +416,14 @@ __global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restr
   // for the count.
   const int rows_now = *d_rows;
   __shared__ float red[16];
-  float* xr = ep.x + (int64_t)r * ep.ldx;
-  const float* pr = ep.part + (int64_t)r * N;
-  const int64_t pst = ep.part_stride;
+  float* xr = x + (int64_t)r * ldx;
+  const float* pr = part + (int64_t)r * N;
   float xv[CPT], gv[CPT], acc[CPT];
 #pragma unroll
   for (int k = 0; k < CPT; ++k) {
     const int c = threadIdx.x + k * NT;
     xv[k] = c < N ? xr[c] : 0.f;
-    gv[k] = c < N ? ep.norm_g[c] : 0.f;
+    gv[k] = c < N ? norm_g[c] : 0.f;
     acc[k] = 0.f;
   }
   for (int s0 = 0; s0 < S; s0 += BATCH) {
@@ -461,7 +465,8 @@ __global__ __launch_bounds__(1024) void k_split_residual_norm(const int* __restr
 // rotated, and written as one 16-byte q piece per half or one 8-byte key piece
 // per half (values: their transposed layout, one element at a time).  Same
 // arithmetic as qkv_store; one wave per 64 quads of a row.
-__global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+__global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_rows, const float* __restrict__ part,
+                                                      int64_t pst, int N, int S, GemmEpi ep) {
   typedef float f4 __attribute__((ext_vector_type(4)));
   constexpr int BATCH = 16;
   const int r = blockIdx.y;
@@ -472,8 +477,8 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
   const int c = (uc >> 2) * 32 + (uc & 3) * 4;
   const int hd = ep.hd, half = hd / 2;
   const int head = c / hd, p = c % hd, d = (p >> 5) * 16 + (p & 15);
-  const f4* pr = reinterpret_cast<const f4*>(ep.part + (int64_t)r * N + c);
-  const int64_t pst4 = ep.part_stride / 4;
+  const f4* pr = reinterpret_cast<const f4*>(part + (int64_t)r * N + c);
+  const int64_t pst4 = pst / 4;
   f4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < S; s0 += BATCH) {
     f4 ta[BATCH], tb[BATCH];
@@ -533,9 +538,12 @@ __global__ __launch_bounds__(64) void k_qkv_epilogue4(const int* __restrict__ d_
 // Sum of split partials + epilogue: one block of 128 threads per (128
 // columns, row).  SPLIT: activation output as hi/lo bf16 planes.
 template <int EPI, int SPLIT, typename KV>
-__global__ __launch_bounds__(128) void k_split_epilogue(const int* __restrict__ d_rows, int N, int S, GemmEpi ep) {
+__global__ __launch_bounds__(128) void k_split_epilogue(const int* __restrict__ d_rows, float* __restrict__ part,
+                                                        int64_t pst, int N, int S, GemmEpi ep) {
   const int r = blockIdx.y;
   const int rows_now = *d_rows;
+  ep.part = part;          // the preloaded copies
+  ep.part_stride = pst;
   if constexpr (EPI == GEMM_EPI_QKV) {
     if (r >= rows_now) return;
   }
@@ -586,8 +594,8 @@ hipError_t launch_tiled(const void* A, int lda, int64_t a_plane, const void* W, 
   // grouped order needs 8 or more row tiles, so it never meets ntw.
 #define RG_TILED_K(E, NTV, XOV)                                                                               \
   hipLaunchKernelGGL((k_gemm_tiled<BM, BN, WM, WN, STAGES, BK, E, NTV, XOV>), grid, dim3(NT), 0, st,           \
-                     (const bf16_t*)A, lda, a_plane, (const bf16_t*)W, ldw, d_rows, rows_ub, N, K, k_per_split, ep, \
-                     gx, gy)
+                     (const bf16_t*)A, (const bf16_t*)W, d_rows, a_plane, lda, ldw, rows_ub, N, K, k_per_split, gx, \
+                     gy, ep)
 #define RG_TILED(E)                                                                                           \
   do {                                                                                                        \
     if constexpr (BM == 256) {                                                                                \
@@ -619,7 +627,9 @@ template <int SPLIT, typename KV>
 hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, const GemmEpi& ep, hipStream_t st) {
   if (ep.mode == GEMM_EPI_RESIDUAL && ep.norm_g) {
     const int cpt = (N + 1023) / 1024;
-#define RG_SRN(C) hipLaunchKernelGGL((k_split_residual_norm<SPLIT, C>), dim3(rows_ub), dim3(1024), 0, st, d_rows, N, S, ep)
+#define RG_SRN(C)                                                                                             \
+  hipLaunchKernelGGL((k_split_residual_norm<SPLIT, C>), dim3(rows_ub), dim3(1024), 0, st, d_rows, ep.part,        \
+                     ep.part_stride, ep.x, ep.norm_g, N, S, ep.ldx, ep)
     if (cpt <= 1) RG_SRN(1);
     else if (cpt <= 2) RG_SRN(2);
     else if (cpt <= 4) RG_SRN(4);
@@ -630,16 +640,29 @@ hipError_t launch_split_epilogue(const int* d_rows, int rows_ub, int N, int S, c
   }
   if constexpr (SPLIT == 1) {
     if (ep.mode == GEMM_EPI_QKV && N % 32 == 0 && ep.hd % 32 == 0 && ep.part_stride % 4 == 0) {
-      hipLaunchKernelGGL(k_qkv_epilogue4, dim3((N / 8 + 63) / 64, rows_ub), dim3(64), 0, st, d_rows, N, S, ep);
+      hipLaunchKernelGGL(k_qkv_epilogue4, dim3((N / 8 + 63) / 64, rows_ub), dim3(64), 0, st, d_rows, ep.part,
+                         ep.part_stride, N, S, ep);
       return hipGetLastError();
     }
   }
   dim3 grid((N + 127) / 128, rows_ub);
   switch (ep.mode) {
-    case GEMM_EPI_STORE: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_STORE, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
-    case GEMM_EPI_RESIDUAL: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_RESIDUAL, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
-    case GEMM_EPI_SWIGLU: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_SWIGLU, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
-    case GEMM_EPI_QKV: hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_QKV, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, N, S, ep); break;
+    case GEMM_EPI_STORE:
+      hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_STORE, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, ep.part,
+                         ep.part_stride, N, S, ep);
+      break;
+    case GEMM_EPI_RESIDUAL:
+      hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_RESIDUAL, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, ep.part,
+                         ep.part_stride, N, S, ep);
+      break;
+    case GEMM_EPI_SWIGLU:
+      hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_SWIGLU, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, ep.part,
+                         ep.part_stride, N, S, ep);
+      break;
+    case GEMM_EPI_QKV:
+      hipLaunchKernelGGL((k_split_epilogue<GEMM_EPI_QKV, SPLIT, KV>), grid, dim3(128), 0, st, d_rows, ep.part,
+                         ep.part_stride, N, S, ep);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
