@@ -221,13 +221,12 @@ template <int BM, int BN, int WM, int WN, int STAGES, int BK, int EPI, bool NTW,
 __global__ __launch_bounds__((BM / (16 * WM)) * (BN / (16 * WN)) * 64) void k_gemm_tiled(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, const int* __restrict__ d_rows, int64_t a_plane,
     int lda, int ldw, int rows_cap, int N, int K, int k_per_split, int gx, int gy, GemmEpi ep) {
-  // (the arguments the first loads need come first: 14 dwords, which the
-  // build preloads into scalar registers at dispatch)
-  // The row count is read first but waited for only after the first K
-  // step's loads are issued: those clamp A rows to the launch's row bound
-  // rows_cap (>= the count; the activation buffer holds that many rows), so
-  // they do not depend on it.  Rows past the count are multiplied, never
-  // stored.
+  // The arguments the first loads need come first (14 dwords, which the
+  // build preloads into scalar registers at dispatch).  The row count is
+  // read first but waited for only after the first K step's loads are
+  // issued: those clamp A rows to the launch's row bound rows_cap (>= the
+  // count; the activation buffer holds that many rows), so they do not
+  // depend on it.  Rows past the count are multiplied, never stored.
   const int rows_now = *d_rows;
   constexpr int WAVES_M = BM / (16 * WM), WAVES_N = BN / (16 * WN);
   constexpr int NT = WAVES_M * WAVES_N * 64;
